@@ -1,0 +1,41 @@
+"""Workload shapes of the coded matrix-multiplication benchmarks.
+
+Shapes follow the paper's experiments in spirit (Sec. III-F draws random dense
+matrices and multiplies them by a vector) at sizes that fill one MI355X.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n: int
+    k: int
+    q: int
+    r: int
+    s: int
+    dtype: str            # "f32" or "bf16": dtype of A, X and the parity coefficients
+    seed: int
+    units: int            # products / calls / decodes / iterations in one run
+    a_std: float = 1.0
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def qb(self) -> int:
+        return -(-self.q // self.k)
+
+
+WORKLOADS = {
+    "mds4x2_2048x512": Workload("mds4x2_2048x512", 4, 2, 2048, 512, 1, "f32", 0, 100,
+                                extra={"seeds": list(range(100))}),
+    "gemv16x12_65536x8192": Workload("gemv16x12_65536x8192", 16, 12, 65536, 8192, 1, "f32", 2, 1000),
+    "gemm_bf16_32x24_131072x16384x64": Workload("gemm_bf16_32x24_131072x16384x64", 32, 24, 131072, 16384,
+                                                64, "bf16", 3, 20),
+    "decode64x48_16384x4096x8": Workload("decode64x48_16384x4096x8", 64, 48, 16384, 4096, 8, "f32", 4, 10000,
+                                         extra={"min_parity": 8}),
+    "gd20x16_262144x4096": Workload("gd20x16_262144x4096", 20, 16, 262144, 4096, 1, "f32", 5, 200,
+                                    a_std=1.0 / 64.0,
+                                    extra={"eta": 0.5, "noise_std": 0.1}),
+}
