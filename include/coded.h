@@ -1,0 +1,221 @@
+/*
+ * coded.h -- C ABI of the MI355X (gfx950) library for (n,k) MDS-coded matrix
+ * multiplication.
+ *
+ * Method: K. Lee, M. Lam, R. Pedarsani, D. Papailiopoulos, K. Ramchandran,
+ * "Speeding Up Distributed Machine Learning Using Codes", IEEE Trans. Inf.
+ * Theory (arXiv 1512.02673), Sec. III.  A data matrix A (q x r) is padded with
+ * zero rows to a multiple of k and split into k row-blocks A_1..A_k of qb =
+ * ceil(q/k) rows.  An (n,k) MDS code with systematic generator G = [I_k; P]
+ * maps them to n coded blocks A'_i = sum_j G[i][j] A_j (A'_i = A_i for i < k).
+ * Worker i computes Y_i = A'_i X; the master recovers A X from ANY k of the n
+ * results by solving G_S B = Y_S and concatenating B (Sec. III-A); the
+ * survivor set S is the k fastest of n workers whose runtimes follow the
+ * shifted-exponential model (Sec. III-B, III-C).  Workers are simulated on
+ * one GPU: all n products run, and the survivor draw picks whose results the
+ * master uses.
+ *
+ * Conventions shared by every call:
+ *  - Worker and block indices are 0-based: workers 0..k-1 hold A_0..A_{k-1}
+ *    (the systematic blocks), workers k..n-1 hold the n-k parity blocks.
+ *  - Matrices are row-major.  A is q x r with row stride lda >= r elements.
+ *    X is r x s with row stride ldx >= s.  out is q x s with row stride ldo.
+ *  - The parity buffer holds the n-k parity blocks, each qb x r, dense (row
+ *    stride r), in `planes` planes: element (p, t, c) of plane h is at
+ *    [h*(n-k)*qb*r + p*qb*r + t*r + c].  With planes == 2 the coded block is
+ *    the exact-sum pair hi + lo: hi is the coded value rounded to the storage
+ *    dtype and lo the rounded remainder, which gives the parity blocks about
+ *    twice the storage precision at (n-k)/n extra bytes.  planes == 1 stores
+ *    hi only.
+ *  - Y (worker results) is n x qb x s, dense: element (i, t, c) at
+ *    [(i*qb + t)*s + c].  Rows t with i*qb + t >= q of systematic blocks are
+ *    the zero padding and hold 0.
+ *  - Device pointers are HIP device memory of the device current when the
+ *    call is made; `stream` is a hipStream_t (NULL = the null stream).
+ *  - Every call that takes a stream only enqueues work on it and returns; no
+ *    call synchronises the device.  Argument errors are found on the host
+ *    before anything is enqueued; they return a status and set a
+ *    thread-local message (coded_last_error).  Numerical singularity of a
+ *    survivor set is found on the device and reported through `info`.
+ *  - The caller owns every buffer.  Apart from the code object made by
+ *    coded_code_create, the library allocates no device memory.
+ *  - Nothing throws across this interface.
+ */
+#ifndef CODED_H
+#define CODED_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum coded_status {
+    CODED_OK = 0,
+    CODED_ERR_ARG = 1,         /* null pointer, bad index, value out of range */
+    CODED_ERR_SHAPE = 2,       /* inconsistent sizes or strides */
+    CODED_ERR_TOO_FEW = 3,     /* fewer than k survivors */
+    CODED_ERR_SINGULAR = 4,    /* reserved: singularity is reported via info */
+    CODED_ERR_HIP = 5,         /* a HIP runtime call failed */
+    CODED_ERR_UNSUPPORTED = 6  /* valid but not implemented (e.g. non-systematic G) */
+} coded_status;
+
+typedef enum coded_dtype {
+    CODED_F32 = 0,
+    CODED_BF16 = 1,            /* bfloat16 bit patterns (uint16) */
+    CODED_F64 = 2
+} coded_dtype;
+
+/* Largest n supported (survivor and worker lists travel as kernel arguments). */
+#define CODED_MAX_N 128
+
+/* Opaque (n,k) code: the generator G on host and device. */
+typedef struct coded_code coded_code;
+
+/*
+ * coded_code_create -- make the code used by every other call (Sec. III-A:
+ * the (n,k) MDS code applied to the k sub-matrices).
+ *   n, k      1 <= k <= n <= CODED_MAX_N.
+ *   G         host, n*k doubles, row-major.  Rows 0..k-1 must be I_k exactly
+ *             (systematic code); otherwise CODED_ERR_UNSUPPORTED.  The caller
+ *             is responsible for G being MDS (every k x k row subset
+ *             invertible); a set that is not invertible is reported at
+ *             decode time through info.
+ *   planes    parity storage planes: 2 (hi + lo, default recipe) or 1.
+ *   out       receives the new code.  The call copies G to the current
+ *             device (one small allocation, synchronous); destroy with
+ *             coded_code_destroy.  Device work that uses the code must be
+ *             finished before destroying it.
+ */
+coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, coded_code** out);
+coded_status coded_code_destroy(coded_code* code);
+coded_status coded_code_info(const coded_code* code, int32_t* n, int32_t* k, int32_t* planes);
+
+/*
+ * coded_sizes -- bytes of the caller-allocated buffers for an A of q x r,
+ * X of r x s, compute dtype dt and worker-result dtype y_dt.
+ *   parity_bytes     the parity buffer (planes * (n-k) * qb * r elements of dt)
+ *   y_bytes          Y (n * qb * s elements of y_dt)
+ *   workspace_bytes  workspace of coded_matmul (its Y, in y_dt = F64 for F32
+ *                    inputs and F32 for BF16 inputs)
+ * Any output pointer may be NULL.
+ */
+coded_status coded_sizes(const coded_code* code, coded_dtype dt, coded_dtype y_dt, int64_t q, int64_t r,
+                         int64_t s, int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes);
+
+/*
+ * coded_encode -- the n-k parity blocks A'_{k+p} = sum_j P[p][j] A_j
+ * (Sec. III-A: the code applied to each element of the sub-matrices; the k
+ * systematic blocks are A itself and are not copied).  Rows of A at or beyond
+ * q are the zero padding of Sec. III-A's footnote and are never read.
+ *   dt        CODED_F32: sums in fp64; CODED_BF16: every P entry must be a
+ *             bfloat16 value (else CODED_ERR_ARG), sums in fp32.
+ *   A         device, q x r of dt, row stride lda.
+ *   parity    device, the parity buffer (layout above), written in full.
+ */
+coded_status coded_encode(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                          void* parity, void* stream);
+
+/*
+ * coded_worker_mm -- the n local products Y_i = A'_i X (Sec. III-A: worker i
+ * multiplies its stored block by the multicast input).  All workers run
+ * unless worker_mask says otherwise.
+ *   A, parity  device, as written by coded_encode for the same q, r, dt.
+ *   X          device, r x s of dt, row stride ldx (s == 1 requires ldx == 1).
+ *   worker_mask host, n bytes or NULL: worker i runs iff mask[i] != 0.
+ *              Rows of Y of workers that do not run are left untouched.
+ *   Y          device, n x qb x s of y_dt (layout above).
+ *   y_dt       CODED_F64 (dt = F32: products accumulate in fp64) or
+ *              CODED_F32 (dt = F32: fp64 accumulate, rounded on store;
+ *              dt = BF16: fp32 accumulate).
+ */
+coded_status coded_worker_mm(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                             const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* worker_mask,
+                             void* Y, coded_dtype y_dt, void* stream);
+
+/*
+ * coded_decode -- dec(indices, results) of Sec. III-A for one survivor set.
+ *   survivors  host, `count` worker indices in arrival order; the first k are
+ *              used (count < k: CODED_ERR_TOO_FEW; an index outside [0,n) or
+ *              a repeat among the first k: CODED_ERR_ARG).  The result does
+ *              not depend on their order.
+ *   Y          device, n x qb x s of y_dt (CODED_F64 or CODED_F32); only the
+ *              survivors' rows are read.
+ *   out        device fp32, q x s, row stride ldo >= s.  Padding rows are not
+ *              written.  Systematic survivors are copied, the missing blocks
+ *              are solved for in fp64 (LU of the survivor sub-matrix of G,
+ *              partial pivoting, systematic rows first).
+ *   info       device int32[1]: set to 0 on success, or j > 0 when pivot j
+ *              of the k x k LU is exactly zero (out is then not written).
+ */
+coded_status coded_decode(const coded_code* code, const int32_t* survivors, int32_t count, const void* Y,
+                          coded_dtype y_dt, int64_t q, int64_t s, float* out, int64_t ldo, int32_t* info,
+                          void* stream);
+
+/*
+ * coded_decode_batched -- coded_decode for `batch` survivor sets at once (one
+ * decode per set, all sharing Y).
+ *   sets       device int32, batch x k, any order within a row.  A row with an
+ *              index outside [0,n) or a repeat gets info = -1 and no output.
+ *   out        device fp32; set b writes q x s at out + b*out_stride, row
+ *              stride ldo.
+ *   info       device int32[batch] (0, -1, or the zero-pivot index).
+ */
+coded_status coded_decode_batched(const coded_code* code, const int32_t* sets, int32_t batch, const void* Y,
+                                  coded_dtype y_dt, int64_t q, int64_t s, float* out, int64_t ldo,
+                                  int64_t out_stride, int32_t* info, void* stream);
+
+/*
+ * coded_draw_survivors -- host only.  The k fastest of n workers in draw
+ * `draw` (Sec. III-B eq. mds_coded; Sec. III-C).  Worker i's mother-runtime
+ * sample is T0 = shift + E/rate, E = -ln U, with U from the 64-bit word
+ * u = SplitMix64 output number (4<<56 | draw<<16 | i) of the generator seeded
+ * with `seed`, U = ((u >> 11) + 0.5) * 2^-53; its task time is T0 / k.  The k
+ * workers with the largest u are the k smallest runtimes (ties to the lower
+ * index), so the set is chosen in integer arithmetic.
+ *   survivors_out  host int32[k], ascending.
+ *   t_overall_out  host, T_(k), the k-th smallest task time (may be NULL).
+ * Requires rate > 0, draw < 2^40.
+ */
+coded_status coded_draw_survivors(int32_t n, int32_t k, uint64_t seed, uint64_t draw, double shift, double rate,
+                                  int32_t* survivors_out, double* t_overall_out);
+
+/*
+ * coded_draw_survivor_sets -- host only.  `batch` distinct survivor sets with
+ * at least min_parity parity workers: draws first_draw, first_draw+1, ... are
+ * taken in order; a set is kept if it qualifies and differs from every set
+ * kept before.  sets_out: host int32[batch*k], each row ascending.
+ * next_draw_out (may be NULL): first draw not consumed.  Fails with
+ * CODED_ERR_ARG if min_parity > min(k, n-k).
+ */
+coded_status coded_draw_survivor_sets(int32_t n, int32_t k, uint64_t seed, uint64_t first_draw, int32_t batch,
+                                      int32_t min_parity, int32_t* sets_out, uint64_t* next_draw_out);
+
+/*
+ * coded_matmul -- one coded product (Sec. III-A protocol): encode (unless
+ * parity_ready), draw the survivors on the host, run all n worker products
+ * into the workspace, decode from the survivors into out.
+ *   dt          CODED_F32 (worker results in fp64) or CODED_BF16 (fp32).
+ *   parity      device parity buffer; written first when parity_ready == 0.
+ *   seed, draw, shift, rate   as coded_draw_survivors.
+ *   survivors_out  host int32[k] (may be NULL); t_overall_out may be NULL.
+ *   workspace   device, coded_sizes' workspace_bytes.
+ *   info        device int32[1], as coded_decode.
+ */
+coded_status coded_matmul(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                          void* parity, int32_t parity_ready, const void* X, int64_t s, int64_t ldx, uint64_t seed,
+                          uint64_t draw, double shift, double rate, int32_t* survivors_out, double* t_overall_out,
+                          float* out, int64_t ldo, void* workspace, int32_t* info, void* stream);
+
+/* Static text of a status code. */
+const char* coded_status_string(coded_status status);
+/* Message of the last failing call on this thread ("" if none). */
+const char* coded_last_error(void);
+/* Library version string. */
+const char* coded_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CODED_H */

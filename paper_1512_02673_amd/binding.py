@@ -1,0 +1,253 @@
+"""ctypes binding of libcoded_mi355x.so: the C ABI's calls under the same names.
+
+Argument marshalling only: shapes, strides and data pointers are read from
+torch tensors, the current torch stream is passed as the HIP stream, and every
+step of the coded product runs in the library.  Loading fails loudly when the
+library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+from .build import LIB_PATH
+
+CODED_OK, CODED_ERR_ARG, CODED_ERR_SHAPE, CODED_ERR_TOO_FEW, CODED_ERR_SINGULAR, CODED_ERR_HIP, \
+    CODED_ERR_UNSUPPORTED = range(7)
+CODED_F32, CODED_BF16, CODED_F64 = 0, 1, 2
+CODED_MAX_N = 128
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "coded.h")
+
+_c_i32, _c_i64, _c_u64, _c_dbl, _c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p
+
+_SIGNATURES = {
+    "coded_code_create": (_c_i32, [_c_i32, _c_i32, _c_p, _c_i32, ctypes.POINTER(_c_p)]),
+    "coded_code_destroy": (_c_i32, [_c_p]),
+    "coded_code_info": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
+    "coded_sizes": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_encode": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p]),
+    "coded_worker_mm": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_p,
+                                 _c_p, _c_i32, _c_p]),
+    "coded_decode": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p]),
+    "coded_decode_batched": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i64,
+                                      _c_p, _c_p]),
+    "coded_draw_survivors": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p]),
+    "coded_draw_survivor_sets": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_i32, _c_i32, _c_p, _c_p]),
+    "coded_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i32, _c_p, _c_i64, _c_i64,
+                              _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_status_string": (ctypes.c_char_p, [_c_i32]),
+    "coded_last_error": (ctypes.c_char_p, []),
+    "coded_version": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+class CodedError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run paper_1512_02673_amd.build.build() "
+                               "(or __graft_entry__.build()) first")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            f = getattr(h, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = h
+    return _lib
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/coded.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(coded_[a-z0-9_]+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    return lib().coded_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().coded_last_error().decode()
+
+
+def version() -> str:
+    return lib().coded_version().decode()
+
+
+def _check(status: int) -> None:
+    if status != CODED_OK:
+        raise CodedError(status, last_error())
+
+
+# ---------------------------------------------------------------- host-only calls
+
+def coded_draw_survivors(n: int, k: int, seed: int, draw: int, shift: float = 1.0, rate: float = 1.0):
+    """(survivors ascending int32[k], T_(k)) of one draw."""
+    out = np.zeros(k, dtype=np.int32)
+    t = ctypes.c_double()
+    _check(lib().coded_draw_survivors(n, k, seed, draw, shift, rate, out.ctypes.data, ctypes.addressof(t)))
+    return out, t.value
+
+
+def coded_draw_survivor_sets(n: int, k: int, seed: int, batch: int, min_parity: int = 0, first_draw: int = 0):
+    """(sets int32[batch, k], next unused draw)."""
+    out = np.zeros((batch, k), dtype=np.int32)
+    nxt = ctypes.c_uint64()
+    _check(lib().coded_draw_survivor_sets(n, k, seed, first_draw, batch, min_parity, out.ctypes.data,
+                                          ctypes.addressof(nxt)))
+    return out, nxt.value
+
+
+# ---------------------------------------------------------------- device calls
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    return {torch.float32: CODED_F32, torch.bfloat16: CODED_BF16, torch.float64: CODED_F64}[t.dtype]
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _matrix(t, name):
+    """(rows, cols, row stride) of a 1-D (column) or row-major 2-D tensor."""
+    if t.dim() == 1:
+        if t.stride(0) != 1:
+            raise ValueError(f"{name} must be contiguous")
+        return t.shape[0], 1, 1
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be 1-D or row-major 2-D")
+    return t.shape[0], t.shape[1], max(t.stride(0), 1)
+
+
+class Code:
+    """An (n,k) code: G = [I_k; P] on host and device (coded_code_create)."""
+
+    def __init__(self, n: int, k: int, G: np.ndarray, planes: int = 2):
+        G = np.ascontiguousarray(G, dtype=np.float64)
+        if G.shape != (n, k):
+            raise ValueError("G must be n x k")
+        h = ctypes.c_void_p()
+        _check(lib().coded_code_create(n, k, G.ctypes.data, planes, ctypes.byref(h)))
+        self.handle = h
+        self.n, self.k, self.planes = n, k, planes
+        self.G = G
+
+    @classmethod
+    def systematic(cls, P: np.ndarray, planes: int = 2) -> "Code":
+        P = np.asarray(P, dtype=np.float64)
+        k = P.shape[1]
+        return cls(k + P.shape[0], k, np.vstack([np.eye(k), P]), planes)
+
+    def qb(self, q: int) -> int:
+        return -(-q // self.k)
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().coded_code_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def coded_sizes(code: Code, dt: int, y_dt: int, q: int, r: int, s: int):
+    pb, yb, wb = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().coded_sizes(code.handle, dt, y_dt, q, r, s, ctypes.addressof(pb), ctypes.addressof(yb),
+                             ctypes.addressof(wb)))
+    return pb.value, yb.value, wb.value
+
+
+def coded_encode(code: Code, A, parity, stream=None) -> None:
+    q, r, lda = _matrix(A, "A")
+    _check(lib().coded_encode(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _stream(stream)))
+
+
+def coded_worker_mm(code: Code, A, parity, X, Y, worker_mask=None, stream=None) -> None:
+    q, r, lda = _matrix(A, "A")
+    rx, s, ldx = _matrix(X, "X")
+    if rx != r:
+        raise ValueError("X must have r rows")
+    mask = None
+    if worker_mask is not None:
+        m = np.ascontiguousarray(worker_mask, dtype=np.uint8)
+        if m.shape != (code.n,):
+            raise ValueError("worker_mask must have n entries")
+        mask = m.ctypes.data_as(ctypes.c_void_p)
+    _check(lib().coded_worker_mm(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _ptr(X), s, ldx,
+                                 mask, _ptr(Y), _dtype_code(Y), _stream(stream)))
+
+
+def coded_decode(code: Code, survivors, Y, q: int, out, info, stream=None) -> None:
+    sv = np.ascontiguousarray(survivors, dtype=np.int32)
+    _, s, ldo = _matrix(out, "out")
+    _check(lib().coded_decode(code.handle, sv.ctypes.data_as(ctypes.c_void_p), len(sv), _ptr(Y), _dtype_code(Y), q,
+                              s, _ptr(out), ldo, _ptr(info), _stream(stream)))
+
+
+def coded_decode_batched(code: Code, sets, Y, q: int, out, info, stream=None) -> None:
+    """sets: device int32 (batch, k); out: (batch, q) or (batch, q, s) float32."""
+    batch = sets.shape[0]
+    if out.dim() == 2:
+        s, ldo = 1, 1
+    else:
+        s, ldo = out.shape[2], out.stride(1)
+    _check(lib().coded_decode_batched(code.handle, _ptr(sets), batch, _ptr(Y), _dtype_code(Y), q, s, _ptr(out), ldo,
+                                      out.stride(0), _ptr(info), _stream(stream)))
+
+
+def coded_matmul(code: Code, A, parity, X, out, workspace, info, seed: int, draw: int, parity_ready: bool = True,
+                 shift: float = 1.0, rate: float = 1.0, stream=None):
+    """One coded product; returns (survivors int32[k], T_(k))."""
+    q, r, lda = _matrix(A, "A")
+    rx, s, ldx = _matrix(X, "X")
+    if rx != r:
+        raise ValueError("X must have r rows")
+    _, so, ldo = _matrix(out, "out")
+    surv = np.zeros(code.k, dtype=np.int32)
+    t = ctypes.c_double()
+    _check(lib().coded_matmul(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), int(bool(parity_ready)),
+                              _ptr(X), s, ldx, seed, draw, shift, rate, surv.ctypes.data_as(ctypes.c_void_p),
+                              ctypes.addressof(t), _ptr(out), ldo, _ptr(workspace), _ptr(info), _stream(stream)))
+    return surv, t.value
+
+
+# ---------------------------------------------------------------- buffer helpers
+
+def alloc_parity(code: Code, q: int, r: int, dtype, device="cuda"):
+    torch = _torch()
+    qb = code.qb(q)
+    return torch.empty((code.planes, code.n - code.k, qb, r), dtype=dtype, device=device)
+
+
+def alloc_y(code: Code, q: int, s: int, dtype, device="cuda"):
+    torch = _torch()
+    return torch.empty((code.n, code.qb(q), s), dtype=dtype, device=device)

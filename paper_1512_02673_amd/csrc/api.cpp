@@ -1,0 +1,411 @@
+// C ABI of the coded matrix-multiplication library: argument checking, code
+// objects, survivor draws and kernel launches.  Every entry point validates
+// on the host before enqueueing anything and never throws.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace coded {
+
+static thread_local std::string g_last_error;
+
+coded_status fail(coded_status st, const std::string& msg) {
+    g_last_error = msg;
+    return st;
+}
+
+coded_status hip_fail(hipError_t e, const char* what) {
+    return fail(CODED_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+namespace {
+
+constexpr size_t kMaxDecodeLds = 60 * 1024;
+
+#define CODED_GUARD_BEGIN try {
+#define CODED_GUARD_END                                                   \
+    }                                                                     \
+    catch (const std::bad_alloc&) {                                       \
+        return fail(CODED_ERR_ARG, "host allocation failed");             \
+    }                                                                     \
+    catch (...) {                                                         \
+        return fail(CODED_ERR_ARG, "unexpected host exception");          \
+    }
+
+coded_status check_code(const coded_code* c) {
+    if (!c) return fail(CODED_ERR_ARG, "code is NULL");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != c->device)
+        return fail(CODED_ERR_ARG, "code was created on device " + std::to_string(c->device) +
+                                       " but device " + std::to_string(dev) + " is current");
+    return CODED_OK;
+}
+
+int64_t block_rows(int64_t q, int k) { return (q + k - 1) / k; }
+
+size_t dtype_size(coded_dtype d) {
+    switch (d) {
+        case CODED_F32: return 4;
+        case CODED_BF16: return 2;
+        case CODED_F64: return 8;
+    }
+    return 0;
+}
+
+bool valid_dtype(coded_dtype d) { return d == CODED_F32 || d == CODED_BF16 || d == CODED_F64; }
+
+coded_status check_dt(coded_dtype dt, coded_dtype y_dt) {
+    if (dt != CODED_F32 && dt != CODED_BF16) return fail(CODED_ERR_ARG, "dt must be CODED_F32 or CODED_BF16");
+    if (dt == CODED_F32 && y_dt != CODED_F64 && y_dt != CODED_F32)
+        return fail(CODED_ERR_ARG, "with dt = CODED_F32, y_dt must be CODED_F64 or CODED_F32");
+    if (dt == CODED_BF16 && y_dt != CODED_F32) return fail(CODED_ERR_ARG, "with dt = CODED_BF16, y_dt must be CODED_F32");
+    return CODED_OK;
+}
+
+coded_status check_ar(int64_t q, int64_t r, int64_t lda) {
+    if (q < 0 || r < 0) return fail(CODED_ERR_SHAPE, "q and r must be >= 0");
+    if (lda < std::max<int64_t>(r, 1)) return fail(CODED_ERR_SHAPE, "lda must be >= max(r, 1)");
+    return CODED_OK;
+}
+
+bool is_bf16_value(double v) {
+    const float f = static_cast<float>(v);
+    if (static_cast<double>(f) != v) return false;
+    uint32_t b;
+    std::memcpy(&b, &f, 4);
+    return (b & 0xFFFFu) == 0;
+}
+
+coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                       void* parity, hipStream_t st) {
+    const int64_t qb = block_rows(q, c->k);
+    if (c->n == c->k || qb == 0 || r == 0) return CODED_OK;
+    if (!A && q > 0) return fail(CODED_ERR_ARG, "A is NULL");
+    if (!parity) return fail(CODED_ERR_ARG, "parity is NULL");
+    if (dt == CODED_BF16) {
+        for (size_t i = static_cast<size_t>(c->k) * c->k; i < c->G.size(); ++i)
+            if (!is_bf16_value(c->G[i]))
+                return fail(CODED_ERR_ARG, "bf16 encode needs every parity coefficient to be a bfloat16 value");
+    }
+    EncodeArgs a{A, parity, c->dG, q, r, lda, qb, c->n, c->k, c->planes};
+    hipError_t e = dt == CODED_F32 ? launch_encode_f32(a, st) : launch_encode_bf16(a, st);
+    if (e != hipSuccess) return hip_fail(e, "encode launch");
+    return CODED_OK;
+}
+
+coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                        const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* mask, void* Y,
+                        coded_dtype y_dt, hipStream_t st) {
+    if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
+    if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
+    if (s == 1 && ldx != 1 && dt == CODED_F32) {
+        // a single column is read as a contiguous vector
+        return fail(CODED_ERR_UNSUPPORTED, "s == 1 needs ldx == 1");
+    }
+    const int64_t qb = block_rows(q, c->k);
+    if (qb == 0 || s == 0) return CODED_OK;
+    if (!Y) return fail(CODED_ERR_ARG, "Y is NULL");
+    if (r > 0) {
+        if (!A && q > 0) return fail(CODED_ERR_ARG, "A is NULL");
+        if (!X) return fail(CODED_ERR_ARG, "X is NULL");
+        if (!parity && c->n > c->k) return fail(CODED_ERR_ARG, "parity is NULL");
+    }
+    WorkerArgs a{};
+    a.A = A;
+    a.parity = parity;
+    a.X = X;
+    a.Y = Y;
+    a.q = q;
+    a.r = r;
+    a.lda = lda;
+    a.qb = qb;
+    a.s = s;
+    a.ldx = ldx;
+    a.n = c->n;
+    a.k = c->k;
+    a.planes = c->planes;
+    a.y_f64 = y_dt == CODED_F64;
+    for (int i = 0; i < c->n; ++i) {
+        if (mask && !mask[i]) continue;
+        if (i < c->k)
+            a.sys_ids[a.n_sys++] = static_cast<uint8_t>(i);
+        else
+            a.par_ids[a.n_par++] = static_cast<uint8_t>(i);
+    }
+    hipError_t e = dt == CODED_F32 ? launch_worker_f32(a, st) : launch_worker_bf16(a, st);
+    if (e != hipSuccess) return hip_fail(e, "worker launch");
+    return CODED_OK;
+}
+
+// First k of `count` survivors: range and repeat checks; returns the sorted set.
+coded_status take_survivors(const coded_code* c, const int32_t* survivors, int32_t count, DecodeSet& set, int& m) {
+    if (!survivors) return fail(CODED_ERR_ARG, "survivors is NULL");
+    if (count < c->k)
+        return fail(CODED_ERR_TOO_FEW, "need k = " + std::to_string(c->k) + " survivors, got " + std::to_string(count));
+    std::vector<int32_t> v(survivors, survivors + c->k);
+    for (int32_t w : v)
+        if (w < 0 || w >= c->n) return fail(CODED_ERR_ARG, "survivor index " + std::to_string(w) + " outside [0, n)");
+    std::sort(v.begin(), v.end());
+    if (std::adjacent_find(v.begin(), v.end()) != v.end()) return fail(CODED_ERR_ARG, "repeated survivor index");
+    std::memset(&set, 0, sizeof(set));
+    m = 0;
+    for (int i = 0; i < c->k; ++i) {
+        set.idx[i] = v[i];
+        m += v[i] >= c->k;
+    }
+    return CODED_OK;
+}
+
+coded_status do_decode_single(const coded_code* c, const DecodeSet& set, int m, const void* Y, coded_dtype y_dt,
+                              int64_t q, int64_t s, float* out, int64_t ldo, int32_t* info, hipStream_t st) {
+    if (y_dt != CODED_F64 && y_dt != CODED_F32) return fail(CODED_ERR_ARG, "y_dt must be CODED_F64 or CODED_F32");
+    if (q < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q and s must be >= 0");
+    if (ldo < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldo must be >= max(s, 1)");
+    if (!info) return fail(CODED_ERR_ARG, "info is NULL");
+    const int64_t qb = block_rows(q, c->k);
+    if (qb * s > 0 && (!Y || !out)) return fail(CODED_ERR_ARG, "Y or out is NULL");
+    if (decode_lds_bytes(c->k, std::max(m, 1)) > kMaxDecodeLds)
+        return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
+    DecodeArgs a{c->dG, Y, out, info, nullptr, q, qb, s, ldo, 0, c->n, c->k, 1, y_dt == CODED_F64};
+    hipError_t e = launch_decode(a, &set, m, st);
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return CODED_OK;
+}
+
+}  // namespace
+}  // namespace coded
+
+using namespace coded;
+
+extern "C" {
+
+coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, coded_code** out) {
+    CODED_GUARD_BEGIN
+    if (!out) return fail(CODED_ERR_ARG, "out is NULL");
+    *out = nullptr;
+    if (!G) return fail(CODED_ERR_ARG, "G is NULL");
+    if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
+    if (planes != 1 && planes != 2) return fail(CODED_ERR_ARG, "planes must be 1 or 2");
+    for (int64_t i = 0; i < static_cast<int64_t>(n) * k; ++i)
+        if (!std::isfinite(G[i])) return fail(CODED_ERR_ARG, "G has a non-finite entry");
+    for (int i = 0; i < k; ++i)
+        for (int j = 0; j < k; ++j)
+            if (G[i * k + j] != (i == j ? 1.0 : 0.0))
+                return fail(CODED_ERR_UNSUPPORTED, "only systematic codes (rows 0..k-1 of G equal to I_k) are supported");
+    auto* c = new coded_code();
+    c->n = n;
+    c->k = k;
+    c->planes = planes;
+    c->G.assign(G, G + static_cast<size_t>(n) * k);
+    hipError_t e = hipGetDevice(&c->device);
+    if (e == hipSuccess) e = hipMalloc(&c->dG, c->G.size() * sizeof(double));
+    if (e == hipSuccess) e = hipMemcpy(c->dG, c->G.data(), c->G.size() * sizeof(double), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        if (c->dG) (void)hipFree(c->dG);
+        delete c;
+        return hip_fail(e, "coded_code_create");
+    }
+    *out = c;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_code_destroy(coded_code* c) {
+    CODED_GUARD_BEGIN
+    if (!c) return CODED_OK;
+    hipError_t e = hipSuccess;
+    if (c->dG) e = hipFree(c->dG);
+    delete c;
+    if (e != hipSuccess) return hip_fail(e, "coded_code_destroy");
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_code_info(const coded_code* c, int32_t* n, int32_t* k, int32_t* planes) {
+    if (!c) return fail(CODED_ERR_ARG, "code is NULL");
+    if (n) *n = c->n;
+    if (k) *k = c->k;
+    if (planes) *planes = c->planes;
+    return CODED_OK;
+}
+
+coded_status coded_sizes(const coded_code* c, coded_dtype dt, coded_dtype y_dt, int64_t q, int64_t r, int64_t s,
+                         int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes) {
+    CODED_GUARD_BEGIN
+    if (!c) return fail(CODED_ERR_ARG, "code is NULL");
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (q < 0 || r < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q, r, s must be >= 0");
+    const int64_t qb = block_rows(q, c->k);
+    if (parity_bytes)
+        *parity_bytes = static_cast<int64_t>(c->planes) * (c->n - c->k) * qb * r * static_cast<int64_t>(dtype_size(dt));
+    if (y_bytes) *y_bytes = static_cast<int64_t>(c->n) * qb * s * static_cast<int64_t>(dtype_size(y_dt));
+    if (workspace_bytes)
+        *workspace_bytes = static_cast<int64_t>(c->n) * qb * s * (dt == CODED_F32 ? 8 : 4);
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_encode(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                          void* parity, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    if (dt != CODED_F32 && dt != CODED_BF16) return fail(CODED_ERR_ARG, "dt must be CODED_F32 or CODED_BF16");
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    return do_encode(c, dt, A, q, r, lda, parity, static_cast<hipStream_t>(stream));
+    CODED_GUARD_END
+}
+
+coded_status coded_worker_mm(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                             const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* worker_mask,
+                             void* Y, coded_dtype y_dt, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    return do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, worker_mask, Y, y_dt, static_cast<hipStream_t>(stream));
+    CODED_GUARD_END
+}
+
+coded_status coded_decode(const coded_code* c, const int32_t* survivors, int32_t count, const void* Y,
+                          coded_dtype y_dt, int64_t q, int64_t s, float* out, int64_t ldo, int32_t* info,
+                          void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    DecodeSet set;
+    int m = 0;
+    if (coded_status st = take_survivors(c, survivors, count, set, m)) return st;
+    return do_decode_single(c, set, m, Y, y_dt, q, s, out, ldo, info, static_cast<hipStream_t>(stream));
+    CODED_GUARD_END
+}
+
+coded_status coded_decode_batched(const coded_code* c, const int32_t* sets, int32_t batch, const void* Y,
+                                  coded_dtype y_dt, int64_t q, int64_t s, float* out, int64_t ldo,
+                                  int64_t out_stride, int32_t* info, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    if (y_dt != CODED_F64 && y_dt != CODED_F32) return fail(CODED_ERR_ARG, "y_dt must be CODED_F64 or CODED_F32");
+    if (batch < 0) return fail(CODED_ERR_ARG, "batch must be >= 0");
+    if (batch == 0) return CODED_OK;
+    if (q < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q and s must be >= 0");
+    if (ldo < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldo must be >= max(s, 1)");
+    if (batch > 1 && out_stride < q * ldo) return fail(CODED_ERR_SHAPE, "out_stride must be >= q * ldo");
+    if (!sets || !info) return fail(CODED_ERR_ARG, "sets or info is NULL");
+    const int64_t qb = block_rows(q, c->k);
+    if (qb * s > 0 && (!Y || !out)) return fail(CODED_ERR_ARG, "Y or out is NULL");
+    const int mmax = std::min(c->k, c->n - c->k);
+    if (decode_lds_bytes(c->k, std::max(mmax, 1)) > kMaxDecodeLds)
+        return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
+    DecodeArgs a{c->dG, Y, out, info, sets, q, qb, s, ldo, out_stride, c->n, c->k, batch, y_dt == CODED_F64};
+    hipError_t e = launch_decode(a, nullptr, mmax, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_draw_survivors(int32_t n, int32_t k, uint64_t seed, uint64_t draw, double shift, double rate,
+                                  int32_t* survivors_out, double* t_overall_out) {
+    CODED_GUARD_BEGIN
+    if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
+    if (!survivors_out) return fail(CODED_ERR_ARG, "survivors_out is NULL");
+    if (!(rate > 0.0) || !std::isfinite(shift)) return fail(CODED_ERR_ARG, "need rate > 0 and a finite shift");
+    if (draw >= (1ull << 40)) return fail(CODED_ERR_ARG, "draw must be < 2^40");
+    const double t = coded_rng::draw_survivors(n, k, seed, draw, shift, rate, survivors_out);
+    if (t_overall_out) *t_overall_out = t;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_draw_survivor_sets(int32_t n, int32_t k, uint64_t seed, uint64_t first_draw, int32_t batch,
+                                      int32_t min_parity, int32_t* sets_out, uint64_t* next_draw_out) {
+    CODED_GUARD_BEGIN
+    if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
+    if (batch < 0) return fail(CODED_ERR_ARG, "batch must be >= 0");
+    if (batch > 0 && !sets_out) return fail(CODED_ERR_ARG, "sets_out is NULL");
+    if (min_parity < 0 || min_parity > std::min(k, n - k))
+        return fail(CODED_ERR_ARG, "min_parity must lie in [0, min(k, n-k)]");
+    std::set<std::vector<int32_t>> seen;
+    std::vector<int32_t> cur(k);
+    uint64_t d = first_draw;
+    int32_t got = 0;
+    while (got < batch) {
+        if (d >= (1ull << 40)) return fail(CODED_ERR_ARG, "ran out of draws");
+        coded_rng::draw_survivors(n, k, seed, d, 1.0, 1.0, cur.data());
+        ++d;
+        int m = 0;
+        for (int32_t w : cur) m += w >= k;
+        if (m < min_parity) continue;
+        if (!seen.insert(cur).second) continue;
+        std::copy(cur.begin(), cur.end(), sets_out + static_cast<int64_t>(got) * k);
+        ++got;
+    }
+    if (next_draw_out) *next_draw_out = d;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                          void* parity, int32_t parity_ready, const void* X, int64_t s, int64_t ldx, uint64_t seed,
+                          uint64_t draw, double shift, double rate, int32_t* survivors_out, double* t_overall_out,
+                          float* out, int64_t ldo, void* workspace, int32_t* info, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    const coded_dtype y_dt = dt == CODED_F32 ? CODED_F64 : CODED_F32;
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
+    if (ldo < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldo must be >= max(s, 1)");
+    if (!info) return fail(CODED_ERR_ARG, "info is NULL");
+    if (!(rate > 0.0) || !std::isfinite(shift)) return fail(CODED_ERR_ARG, "need rate > 0 and a finite shift");
+    if (draw >= (1ull << 40)) return fail(CODED_ERR_ARG, "draw must be < 2^40");
+    const int64_t qb = block_rows(q, c->k);
+    if (qb * s > 0 && (!workspace || !out)) return fail(CODED_ERR_ARG, "workspace or out is NULL");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    // Survivors first: a host-only step, so a bad argument enqueues nothing.
+    int32_t surv[CODED_MAX_N];
+    const double t = coded_rng::draw_survivors(c->n, c->k, seed, draw, shift, rate, surv);
+    DecodeSet set;
+    int m = 0;
+    if (coded_status s2 = take_survivors(c, surv, c->k, set, m)) return s2;
+    if (decode_lds_bytes(c->k, std::max(m, 1)) > kMaxDecodeLds)
+        return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
+    if (s == 1 && ldx != 1 && dt == CODED_F32) return fail(CODED_ERR_UNSUPPORTED, "s == 1 needs ldx == 1");
+    if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
+
+    if (!parity_ready)
+        if (coded_status s2 = do_encode(c, dt, A, q, r, lda, parity, st)) return s2;
+    if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, workspace, y_dt, st)) return s2;
+    if (coded_status s2 = do_decode_single(c, set, m, workspace, y_dt, q, s, out, ldo, info, st)) return s2;
+    if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
+    if (t_overall_out) *t_overall_out = t;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+const char* coded_status_string(coded_status status) {
+    switch (status) {
+        case CODED_OK: return "CODED_OK";
+        case CODED_ERR_ARG: return "CODED_ERR_ARG";
+        case CODED_ERR_SHAPE: return "CODED_ERR_SHAPE";
+        case CODED_ERR_TOO_FEW: return "CODED_ERR_TOO_FEW";
+        case CODED_ERR_SINGULAR: return "CODED_ERR_SINGULAR";
+        case CODED_ERR_HIP: return "CODED_ERR_HIP";
+        case CODED_ERR_UNSUPPORTED: return "CODED_ERR_UNSUPPORTED";
+    }
+    return "unknown coded_status";
+}
+
+const char* coded_last_error(void) { return g_last_error.c_str(); }
+
+const char* coded_version(void) { return "coded-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"

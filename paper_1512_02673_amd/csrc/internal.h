@@ -1,0 +1,82 @@
+// Internal declarations shared by the host glue and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/coded.h"
+
+struct coded_code {
+    int32_t n = 0, k = 0, planes = 2;
+    std::vector<double> G;     // host copy, n*k row-major
+    double* dG = nullptr;      // device copy, n*k row-major
+    int device = 0;
+};
+
+namespace coded {
+
+constexpr int kMaxN = CODED_MAX_N;
+
+// Status plumbing: every API function funnels its failures through fail().
+coded_status fail(coded_status st, const std::string& msg);
+coded_status hip_fail(hipError_t e, const char* what);
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------- encode
+struct EncodeArgs {
+    const void* A;        // q x r, row stride lda (f32 or bf16 bits)
+    void* parity;         // planes x (n-k) x qb x r
+    const double* G;      // device n x k
+    int64_t q, r, lda, qb;
+    int32_t n, k, planes;
+};
+hipError_t launch_encode_f32(const EncodeArgs& a, hipStream_t st);
+hipError_t launch_encode_bf16(const EncodeArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- workers
+struct WorkerArgs {
+    const void* A;        // q x r, row stride lda
+    const void* parity;   // planes x (n-k) x qb x r
+    const void* X;        // r x s, row stride ldx
+    void* Y;              // n x qb x s
+    int64_t q, r, lda, qb, s, ldx;
+    int32_t n, k, planes;
+    int32_t y_f64;        // 1: Y is fp64, 0: Y is fp32
+    int32_t n_sys, n_par; // active systematic / parity workers
+    uint8_t sys_ids[kMaxN];
+    uint8_t par_ids[kMaxN];
+};
+hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st);
+hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- decode
+struct DecodeSet {
+    int32_t idx[kMaxN];
+};
+struct DecodeArgs {
+    const double* G;      // device n x k
+    const void* Y;        // n x qb x s
+    float* out;           // batch x (q x s, row stride ldo), set stride out_stride
+    int32_t* info;        // batch
+    const int32_t* sets;  // device batch x k, or null when `single` is used
+    int64_t q, qb, s, ldo, out_stride;
+    int32_t n, k, batch, y_f64;
+};
+// LDS bytes of the decode kernel's matrices for k survivors and at most mmax
+// missing blocks; launch_decode sizes its dynamic LDS with it.
+size_t decode_lds_bytes(int k, int mmax);
+hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax, hipStream_t st);
+
+}  // namespace coded
+
+// Host runtime model (survivors.cpp); plain C++, no device code.
+namespace coded_rng {
+uint64_t splitmix64_output(uint64_t seed, uint64_t index);
+uint64_t runtime_word(uint64_t seed, uint64_t stream, uint64_t draw, uint64_t worker);
+// Survivors of one draw: k worker indices ascending; returns T_(k).
+double draw_survivors(int n, int k, uint64_t seed, uint64_t draw, double shift, double rate, int32_t* out);
+}  // namespace coded_rng

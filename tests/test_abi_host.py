@@ -1,0 +1,76 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every function the header declares, and its host logic (the survivor draw)
+agrees bit for bit with the oracle."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle import coded as oc
+
+
+def test_library_exports_every_header_function(lib):
+    names = lib.header_functions()
+    assert len(names) >= 14
+    h = lib.lib()
+    for name in names:
+        assert hasattr(h, name), name
+    assert "gfx950" in lib.version()
+
+
+def test_status_strings(lib):
+    for code, name in [(lib.CODED_OK, "CODED_OK"), (lib.CODED_ERR_ARG, "CODED_ERR_ARG"),
+                       (lib.CODED_ERR_TOO_FEW, "CODED_ERR_TOO_FEW"), (lib.CODED_ERR_HIP, "CODED_ERR_HIP"),
+                       (lib.CODED_ERR_UNSUPPORTED, "CODED_ERR_UNSUPPORTED")]:
+        assert lib.status_string(code) == name
+
+
+@pytest.mark.parametrize("n,k,seed", [(4, 2, 0), (4, 2, 17), (16, 12, 2), (32, 24, 3), (64, 48, 4), (20, 16, 5),
+                                      (128, 100, 9), (5, 5, 1), (7, 1, 8)])
+def test_survivor_draw_matches_oracle_bit_exact(lib, n, k, seed):
+    for d in list(range(60)) + [2 ** 39 + 5, 123456789]:
+        got, t = lib.coded_draw_survivors(n, k, seed, d)
+        want, t_ref = oc.draw_survivors(n, k, seed, d)
+        assert np.array_equal(got, want), (d, got, want)
+        assert t == pytest.approx(t_ref, rel=1e-15)
+
+
+def test_survivor_draw_shift_rate(lib):
+    for d in range(20):
+        got, t = lib.coded_draw_survivors(10, 5, 7, d, 2.0, 0.5)
+        want, t_ref = oc.draw_survivors(10, 5, 7, d, 2.0, 0.5)
+        assert np.array_equal(got, want)
+        assert t == pytest.approx(t_ref, rel=1e-15)
+
+
+def test_survivor_sets_match_oracle(lib):
+    got, nxt = lib.coded_draw_survivor_sets(64, 48, 4, 500, min_parity=8)
+    want, nxt_ref = oc.draw_survivor_sets(64, 48, 4, 500, min_parity=8)
+    assert np.array_equal(got, want) and nxt == nxt_ref
+    got, nxt = lib.coded_draw_survivor_sets(4, 2, 0, 6, min_parity=0)
+    want, nxt_ref = oc.draw_survivor_sets(4, 2, 0, 6, min_parity=0)     # all C(4,2) sets
+    assert np.array_equal(got, want) and nxt == nxt_ref
+
+
+def test_host_argument_errors(lib):
+    with pytest.raises(lib.CodedError) as e:
+        lib.coded_draw_survivors(4, 5, 0, 0)
+    assert e.value.status == lib.CODED_ERR_ARG
+    with pytest.raises(lib.CodedError):
+        lib.coded_draw_survivors(4, 2, 0, 0, 1.0, 0.0)          # rate must be > 0
+    with pytest.raises(lib.CodedError):
+        lib.coded_draw_survivors(4, 2, 0, 2 ** 40)              # draw field is 40 bits
+    with pytest.raises(lib.CodedError):
+        lib.coded_draw_survivor_sets(8, 6, 0, 3, min_parity=3)  # at most n-k parity survivors
+    h = lib.lib()
+    # NULL pointers are rejected, not dereferenced
+    assert h.coded_draw_survivors(4, 2, 0, 0, 1.0, 1.0, None, None) == lib.CODED_ERR_ARG
+    assert h.coded_code_create(4, 2, None, 2, ctypes.byref(ctypes.c_void_p())) == lib.CODED_ERR_ARG
+    G = np.vstack([np.eye(2), np.ones((2, 2))])
+    G[0, 1] = 0.5                                               # not systematic
+    assert h.coded_code_create(4, 2, G.ctypes.data, 2, ctypes.byref(ctypes.c_void_p())) == \
+        lib.CODED_ERR_UNSUPPORTED
+    assert h.coded_code_create(4, 2, np.eye(4, 2).ctypes.data, 3, ctypes.byref(ctypes.c_void_p())) == \
+        lib.CODED_ERR_ARG
+    assert h.coded_encode(None, 0, None, 0, 0, 1, None, None) == lib.CODED_ERR_ARG
+    assert h.coded_decode(None, None, 0, None, 2, 0, 0, None, 1, None, None) == lib.CODED_ERR_ARG
