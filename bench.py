@@ -166,13 +166,13 @@ def gemv_workload(args):
         "gemv_ms_p5_p95": [float(np.percentile(gemv_ms, 5)), float(np.percentile(gemv_ms, 95))],
         "decode_ms_mean": float(dec_ms.mean()),
         "coded_matmul_ms_per_call": matmul_ms,
-        "roofline": {"bound": "hbm", "kernel": "gemv_f32_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "algorithmic_bytes_per_launch": algo_bytes,
                      "traffic": traffic, "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE)"},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline_gemv(w, A, P, xs, W, out, args.cpu_products)
+        result["cpu_baseline"] = cpu_baseline_gemv(w, A, P, xs, W, out, min(args.cpu_products, K))
     return result
 
 
@@ -221,7 +221,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192", choices=["gemv16x12_65536x8192"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-products", type=int, default=20)
+    ap.add_argument("--cpu-products", type=int, default=300)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     args = ap.parse_args()
     if args.gpus != 1:

@@ -6,14 +6,12 @@
 // are never read).  A parity block is `planes` planes (hi, lo) in the parity
 // buffer; its product is sum_h plane_h X.
 //
-// The work unit of a wavefront is R consecutive "plane rows": rows of a
-// systematic block, or (row, plane) pairs of a parity block taken row-major,
-// so every wavefront streams the same number of bytes whatever block it
-// serves.  Lanes split the row's columns in 16-byte vectors (64 lanes x 16 B
-// per load instruction, fully coalesced); each lane multiplies in fp64 (the
-// product of two fp32 values is exact in fp64) and the 64 partial sums of a
-// row are combined with cross-lane shuffles.  The kernel is bound by HBM: a
-// row is read exactly once, X (at most a few hundred KB) stays in L2.
+// The single-vector case (s == 1) is the HBM-bound GEMV: every byte of A and
+// of the parity planes is read exactly once, in 16-byte non-temporal loads
+// that a whole workgroup issues over one contiguous stretch of a row at a time
+// (streaming each row through a single wavefront instead measurably loses
+// bandwidth).  Products of two fp32 values are exact in fp64 and are summed
+// in fp64.  s > 1 and unaligned shapes take a general kernel.
 #include "internal.h"
 
 namespace coded {
@@ -92,89 +90,103 @@ __device__ inline void store_y(const WorkerArgs& a, int worker, int64_t t, int64
         static_cast<float*>(a.Y)[off] = static_cast<float>(v);
 }
 
-// s == 1, 16-byte vectors.  R plane rows per wave, U vectors per lane in flight per row.
-template <int R, int U>
-__global__ __launch_bounds__(kThreads) void gemv_f32_kernel(WorkerArgs a) {
+// s == 1, 16-byte vectors.  A workgroup of NT threads owns a tile of T
+// consecutive rows of one worker's block and sweeps it one row at a time:
+// thread tid covers column slots c = tid*4 + j*NT*4 (j < XR) of every row, so
+// each load instruction of the workgroup reads NT*16 contiguous bytes, and
+// its slice of x stays in registers for all T rows.  Rows wider than
+// NT*4*XR are swept in column chunks (x reloaded per chunk).  A parity row's
+// planes (hi, lo) are summed into the same fp64 accumulator.  Partial sums
+// are combined across lanes (shuffles) and waves (LDS) in a fixed order.
+template <int T, int XR, int NT>
+__global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
+    constexpr int NW = NT / 64;
+    constexpr int kChunk = NT * 4 * XR;
+    __shared__ double red[NW][T];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int64_t groups = ceil_div(a.qb, T);
+    const int64_t nsys = groups * a.n_sys;
+    const int64_t g = blockIdx.x;
     int worker;
-    int64_t idx;
+    int64_t grp;
     bool parity;
-    if (!wave_task(a, ceil_div(a.qb, R), ceil_div(a.qb * a.planes, R), worker, idx, parity)) return;
-    const int64_t pr0 = idx * R;
-    const int lane = threadIdx.x & 63;
-
-    const float* rp[R];
-    int64_t rt[R];
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-        RowRef ref = plane_row(a, worker, pr0 + i, parity);
-        rp[i] = ref.ptr;
-        rt[i] = ref.t;
+    if (g < nsys) {
+        worker = a.sys_ids[g / groups];
+        grp = g % groups;
+        parity = false;
+    } else {
+        if (g - nsys >= groups * a.n_par) return;
+        worker = a.par_ids[(g - nsys) / groups];
+        grp = (g - nsys) % groups;
+        parity = true;
     }
+    const int64_t t0 = grp * T;
+    const int nplanes = parity ? a.planes : 1;
+    const int64_t plane = static_cast<int64_t>(a.n - a.k) * a.qb * a.r;
     const float* x = static_cast<const float*>(a.X);
 
-    double acc[R];
+    // Row pointers of the tile (null: padding row or beyond the block).
+    const float* rows[T][2];
 #pragma unroll
-    for (int i = 0; i < R; ++i) acc[i] = 0.0;
-
-    constexpr int kStep = 64 * 4 * U;                 // columns per iteration
-    const int64_t full = (a.r / kStep) * kStep;
-    for (int64_t c0 = 0; c0 < full; c0 += kStep) {
-        float4 xv[U];
-        float4 av[R][U];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            xv[u] = *reinterpret_cast<const float4*>(x + c0 + u * 256 + lane * 4);
-#pragma unroll
-        for (int i = 0; i < R; ++i) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (rp[i])
-                    av[i][u] = load_stream(rp[i] + c0 + u * 256 + lane * 4);
-                else
-                    av[i][u] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const double x0 = xv[u].x, x1 = xv[u].y, x2 = xv[u].z, x3 = xv[u].w;
-#pragma unroll
-            for (int i = 0; i < R; ++i) {
-                acc[i] = fma(static_cast<double>(av[i][u].x), x0, acc[i]);
-                acc[i] = fma(static_cast<double>(av[i][u].y), x1, acc[i]);
-                acc[i] = fma(static_cast<double>(av[i][u].z), x2, acc[i]);
-                acc[i] = fma(static_cast<double>(av[i][u].w), x3, acc[i]);
-            }
-        }
-    }
-    // Tail: remaining columns, one vector per lane per step.
-    for (int64_t c = full + lane * 4; c < a.r; c += 256) {
-        const float4 xv = *reinterpret_cast<const float4*>(x + c);
-        const double x0 = xv.x, x1 = xv.y, x2 = xv.z, x3 = xv.w;
-#pragma unroll
-        for (int i = 0; i < R; ++i) {
-            if (rp[i]) {
-                const float4 v = *reinterpret_cast<const float4*>(rp[i] + c);
-                acc[i] = fma(static_cast<double>(v.x), x0, acc[i]);
-                acc[i] = fma(static_cast<double>(v.y), x1, acc[i]);
-                acc[i] = fma(static_cast<double>(v.z), x2, acc[i]);
-                acc[i] = fma(static_cast<double>(v.w), x3, acc[i]);
-            }
-        }
-    }
-#pragma unroll
-    for (int i = 0; i < R; ++i) acc[i] = wave_sum(acc[i]);
-
-    if (lane == 0) {
-        if (!parity || a.planes == 1) {
-#pragma unroll
-            for (int i = 0; i < R; ++i)
-                if (rt[i] < a.qb) store_y(a, worker, rt[i], 0, acc[i]);
+    for (int i = 0; i < T; ++i) {
+        const int64_t t = t0 + i;
+        rows[i][0] = rows[i][1] = nullptr;
+        if (t >= a.qb) continue;
+        if (!parity) {
+            const int64_t rr = static_cast<int64_t>(worker) * a.qb + t;
+            if (rr < a.q) rows[i][0] = static_cast<const float*>(a.A) + rr * a.lda;
         } else {
-            // planes == 2 and R even: plane rows (2t, 2t+1) are (hi, lo) of row t.
-#pragma unroll
-            for (int i = 0; i < R; i += 2)
-                if (rt[i] < a.qb) store_y(a, worker, rt[i], 0, acc[i] + acc[i + 1]);
+            const float* base = static_cast<const float*>(a.parity) + (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
+            rows[i][0] = base;
+            if (nplanes == 2) rows[i][1] = base + plane;
         }
+    }
+
+    double acc[T];
+#pragma unroll
+    for (int i = 0; i < T; ++i) acc[i] = 0.0;
+
+    for (int64_t cb = 0; cb < a.r; cb += kChunk) {
+        float4 xv[XR];
+#pragma unroll
+        for (int j = 0; j < XR; ++j) {
+            const int64_t c = cb + tid * 4 + j * NT * 4;
+            xv[j] = c < a.r ? *reinterpret_cast<const float4*>(x + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < T; ++i) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float* row = rows[i][h];
+                if (!row) continue;
+                float4 av[XR];
+#pragma unroll
+                for (int j = 0; j < XR; ++j) {
+                    const int64_t c = cb + tid * 4 + j * NT * 4;
+                    av[j] = c < a.r ? load_stream(row + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int j = 0; j < XR; ++j) {
+                    acc[i] = fma(static_cast<double>(av[j].x), static_cast<double>(xv[j].x), acc[i]);
+                    acc[i] = fma(static_cast<double>(av[j].y), static_cast<double>(xv[j].y), acc[i]);
+                    acc[i] = fma(static_cast<double>(av[j].z), static_cast<double>(xv[j].z), acc[i]);
+                    acc[i] = fma(static_cast<double>(av[j].w), static_cast<double>(xv[j].w), acc[i]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        const double v = wave_sum(acc[i]);
+        if (lane == 0) red[wv][i] = v;
+    }
+    __syncthreads();
+    if (tid < T) {
+        double v = 0.0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += red[w][tid];
+        const int64_t t = t0 + tid;
+        if (t < a.qb) store_y(a, worker, t, 0, v);
     }
 }
 
@@ -278,13 +290,35 @@ hipError_t launch_waves(K kernel, const WorkerArgs& a, int64_t wsys, int64_t wpa
 
 }  // namespace
 
+template <int T, int XR>
+hipError_t launch_gemv_wg(const WorkerArgs& a, hipStream_t st) {
+    const int64_t blocks = ceil_div(a.qb, T) * (a.n_sys + a.n_par);
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int XR>
+hipError_t launch_gemv_t(const WorkerArgs& a, hipStream_t st) {
+    // Four rows per workgroup unless that leaves too few workgroups to fill
+    // the chip (256 CUs); then fewer.
+    const int64_t workers = a.n_sys + a.n_par;
+    if (ceil_div(a.qb, 4) * workers >= 4096) return launch_gemv_wg<4, XR>(a, st);
+    if (ceil_div(a.qb, 2) * workers >= 4096) return launch_gemv_wg<2, XR>(a, st);
+    return launch_gemv_wg<1, XR>(a, st);
+}
+
 hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st) {
     if (a.qb == 0) return hipSuccess;
     const bool vec = a.s == 1 && a.ldx == 1 && (a.r % 4 == 0) && (a.lda % 4 == 0) && aligned(a.A, 16) &&
                      aligned(a.X, 16) && (a.parity == nullptr || aligned(a.parity, 16));
     if (vec) {
-        constexpr int R = 4, U = 4;   // R even keeps a parity row's hi and lo in one wave
-        return launch_waves(gemv_f32_kernel<R, U>, a, ceil_div(a.qb, R), ceil_div(a.qb * a.planes, R), st);
+        // Column slots per thread: the whole row in registers up to 8192 columns.
+        if (a.r > 4096) return launch_gemv_t<8>(a, st);
+        if (a.r > 2048) return launch_gemv_t<4>(a, st);
+        if (a.r > 1024) return launch_gemv_t<2>(a, st);
+        return launch_gemv_t<1>(a, st);
     }
     return launch_waves(gemm_small_f32_kernel<4>, a, a.qb, a.qb, st);
 }
