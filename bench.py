@@ -203,6 +203,88 @@ def cpu_baseline_gemv(w, A, P, xs, first, out_dev, products):
             "encode_s": t_enc, "gpu_vs_oracle_max_rel_err": worst}
 
 
+def decode_workload(args):
+    """Decode-heavy workload: (64,48) code, A 16384 x 4096 fp32, X 4096 x 8; the
+    64 worker products are computed once, then one step decodes A X from each
+    of 10000 distinct survivor sets (each with >= 8 parity survivors) in one
+    batched launch.  Unit: one decoded A X."""
+    import torch
+
+    from paper_1512_02673_amd import binding as lib
+
+    w = synth.WORKLOADS["decode64x48_16384x4096x8"]
+    n, k, q, r, s, seed, B = w.n, w.k, w.q, w.r, w.s, w.seed, w.units
+    K, W = args.steps, args.warmup
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    X = synth.gaussian((r, s), seed, synth.STREAM_X)
+    P = synth.parity_matrix(n, k, seed)
+    code = lib.Code.systematic(P, planes=2)
+    dA, dX = torch.from_numpy(A).cuda(), torch.from_numpy(X).cuda()
+    par = lib.alloc_parity(code, q, r, torch.float32)
+    Y = lib.alloc_y(code, q, s, torch.float64)
+    lib.coded_encode(code, dA, par)
+    lib.coded_worker_mm(code, dA, par, dX, Y)
+    sets, _ = lib.coded_draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
+    dsets = torch.from_numpy(sets).cuda()
+    out = torch.empty((B, q, s), dtype=torch.float32, device="cuda")
+    info = torch.zeros(B, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(W):
+        lib.coded_decode_batched(code, dsets, Y, q, out, info)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    start = time.perf_counter()
+    for i in range(K):
+        evs[i][0].record(stream)
+        lib.coded_decode_batched(code, dsets, Y, q, out, info)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - start
+    if int(info.abs().sum().item()) != 0:
+        raise RuntimeError("a decode reported a singular or invalid survivor set")
+    ms = np.array([a.elapsed_time(b) for a, b in evs])
+    qb = code.qb(q)
+    m = (sets >= k).sum(axis=1)
+    algo_bytes = 4.0 * B * q * s + 8.0 * n * qb * s + 4.0 * B * k + 4.0 * B
+    flops = float(np.sum(2.0 * m * k * qb * s))
+    mean_s = float(ms.mean()) * 1e-3
+    achieved = algo_bytes / mean_s / 1e9
+    result = {
+        "metric": METRIC, "value": B * K / elapsed, "unit": "decodes/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "s": s, "sets_per_step": B,
+                   "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean())},
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
+                     "traffic": None, "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)
+    return result
+
+
+def cpu_baseline_decode(w, A, X, P, sets, out_dev, count):
+    """The fp64 oracle decoding a sample of the same survivor sets from its own worker products."""
+    from oracle import coded as oc
+
+    G = oc.systematic_generator(P)
+    Yo = oc.worker_products(oc.encode(G, oc.pad_and_split(A, w.k)), X)
+    idx = np.linspace(0, len(sets) - 1, count).astype(int)
+    worst = 0.0
+    t0 = time.perf_counter()
+    refs = [oc.decode_from_all(G, sets[b], Yo, w.q) for b in idx]
+    t = time.perf_counter() - t0
+    for b, ref in zip(idx, refs):
+        got = out_dev[b].cpu().numpy().astype(np.float64)
+        den = np.max(np.abs(ref), axis=0)
+        worst = max(worst, float(np.max(np.max(np.abs(got - ref), axis=0) / den)))
+    return {"value": count / t, "unit": "decodes/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{w.name}: {count} of the {len(sets)} survivor sets decoded by the oracle (LU of G_S, "
+                      f"solve for all block rows) in {t:.1f} s; encode and worker products not timed",
+            "gpu_vs_oracle_max_rel_err": worst}
+
+
 def calibrate_copy(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -219,9 +301,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="gemv16x12_65536x8192", choices=["gemv16x12_65536x8192"])
+    ap.add_argument("--workload", default="gemv16x12_65536x8192",
+                    choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-products", type=int, default=300)
+    ap.add_argument("--cpu-decodes", type=int, default=1000)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -237,7 +321,14 @@ def main():
     from paper_1512_02673_amd import build as _build
     if not os.path.exists(_build.LIB_PATH):
         _build.build()
-    result = gemv_workload(args)
+    if args.workload == "decode64x48_16384x4096x8":
+        if "--steps" not in sys.argv:
+            args.steps = 20
+        if "--warmup" not in sys.argv:
+            args.warmup = 3
+        result = decode_workload(args)
+    else:
+        result = gemv_workload(args)
     print(json.dumps(result), flush=True)
 
 

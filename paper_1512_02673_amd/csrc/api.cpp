@@ -27,7 +27,7 @@ coded_status hip_fail(hipError_t e, const char* what) {
 
 namespace {
 
-constexpr size_t kMaxDecodeLds = 60 * 1024;
+constexpr size_t kMaxDecodeLds = 56 * 1024;   // dynamic part; static LDS adds under 5 KB
 
 #define CODED_GUARD_BEGIN try {
 #define CODED_GUARD_END                                                   \
@@ -159,7 +159,7 @@ coded_status take_survivors(const coded_code* c, const int32_t* survivors, int32
     std::memset(&set, 0, sizeof(set));
     m = 0;
     for (int i = 0; i < c->k; ++i) {
-        set.idx[i] = v[i];
+        set.packed[i / 4] |= static_cast<uint32_t>(v[i]) << (8 * (i % 4));
         m += v[i] >= c->k;
     }
     return CODED_OK;

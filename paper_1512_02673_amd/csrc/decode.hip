@@ -16,10 +16,16 @@
 // survivors are copied.  Survivors are canonicalised by sorting, so the
 // result does not depend on the order in which they were given.
 //
-// Grid: (chunks of block-row elements, survivor sets).  Every workgroup of a
-// set rebuilds the same D (it is tiny next to the apply) so no global
-// scratch or second launch is needed; the arithmetic is identical in every
-// workgroup, so results are deterministic.
+// Grid: (survivor set, chunk of block-row elements), flattened.  Every
+// workgroup of a set rebuilds the same D (it is small next to the apply), so
+// no global scratch or second launch is needed; the arithmetic is identical
+// in every workgroup, so results are deterministic.
+//
+// Apply: a thread takes E consecutive elements of a block row (E = 4 when a
+// row's columns come in aligned groups of four, so every output goes out as
+// one 16-byte store; E = 1 otherwise, lanes on consecutive elements) and
+// computes the missing outputs PASS at a time in registers; each pair of D
+// entries read from LDS feeds 2*E fused multiply-adds.
 #include "internal.h"
 
 namespace coded {
@@ -27,20 +33,66 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// MAXM: register bound on m (a template bucket); ST (>= every m of the
-// launch) is the row stride of the LDS matrices, sized on the host.
-template <int MAXM, typename YT>
+__device__ inline int set_entry(const DecodeSet& s, int c) {
+    // Pick byte c of the packed set with constant-index reads of the argument.
+    uint32_t word = 0;
+#pragma unroll
+    for (int i = 0; i < kMaxN / 4; ++i) word = (c / 4 == i) ? s.packed[i] : word;
+    return static_cast<int>((word >> (8 * (c % 4))) & 0xFFu);
+}
+
+template <int E, typename YT>
+struct Vec;
+template <>
+struct Vec<1, double> {
+    __device__ static void load(const double* p, double* y) { y[0] = p[0]; }
+};
+template <>
+struct Vec<4, double> {
+    __device__ static void load(const double* p, double* y) {
+        const double2 lo = reinterpret_cast<const double2*>(p)[0], hi = reinterpret_cast<const double2*>(p)[1];
+        y[0] = lo.x; y[1] = lo.y; y[2] = hi.x; y[3] = hi.y;
+    }
+};
+template <>
+struct Vec<1, float> {
+    __device__ static void load(const float* p, double* y) { y[0] = p[0]; }
+};
+template <>
+struct Vec<4, float> {
+    __device__ static void load(const float* p, double* y) {
+        const float4 v = *reinterpret_cast<const float4*>(p);
+        y[0] = v.x; y[1] = v.y; y[2] = v.z; y[3] = v.w;
+    }
+};
+
+template <int E>
+__device__ inline void store_out(float* p, const double* v) {
+    if constexpr (E == 4)
+        *reinterpret_cast<float4*>(p) = make_float4(static_cast<float>(v[0]), static_cast<float>(v[1]),
+                                                    static_cast<float>(v[2]), static_cast<float>(v[3]));
+    else
+        p[0] = static_cast<float>(v[0]);
+}
+
+// PASS: missing outputs computed per sweep over the survivors (register
+// bucket); E: elements per thread; ST (>= every m of the launch, even) is the
+// row stride of the LDS matrices, sized on the host.
+template <int PASS, int E, typename YT>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
-                                                          int64_t elems_per_block, int ST) {
+                                                          int elems_per_block, int ST) {
     __shared__ int32_t sRaw[kMaxN];
-    __shared__ int32_t sS[kMaxN];       // sorted survivors
+    __shared__ int32_t sS[kMaxN];        // sorted survivors
     __shared__ int32_t sPresent[kMaxN];
-    __shared__ int32_t sMiss[MAXM];     // missing systematic blocks, ascending
+    __shared__ int32_t sMiss[kMaxN];     // missing systematic blocks, ascending
+    __shared__ int64_t sYoff[kMaxN];     // element offset of survivor c's result in Y
+    __shared__ int64_t sOoff[kMaxN];     // element offset of block j's first row in out
+    __shared__ int32_t sLim[kMaxN];      // rows of block j that lie inside A (the rest is padding)
     __shared__ int32_t sStatus, sM;
-    __shared__ double sL[MAXM];
-    extern __shared__ double dyn[];
-    double* sD = dyn;                   // D column-major: sD[c * ST + b], c < k
-    double* sMat = dyn + a.k * ST;      // m x m, row stride ST
+    extern __shared__ __align__(16) double dyn[];
+    double* sD = dyn;                    // D column-major: sD[c * ST + b], c < k
+    double* sMat = dyn + a.k * ST;       // m x m, row stride ST
+    double* sL = sMat + ST * ST;         // multipliers of one elimination step
 
     const int tid = threadIdx.x;
     const int n = a.n, k = a.k;
@@ -50,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
 
     if (tid == 0) sStatus = 0;
     for (int i = tid; i < n; i += kThreads) sPresent[i] = 0;
-    for (int c = tid; c < k; c += kThreads) sRaw[c] = a.sets ? a.sets[b * k + c] : single.idx[c];
+    for (int c = tid; c < k; c += kThreads) sRaw[c] = a.sets ? a.sets[b * k + c] : set_entry(single, c);
     __syncthreads();
 
     // Validate (range, repeats), sort by rank, mark present workers.
@@ -83,24 +135,31 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
             if (!sPresent[j]) sMiss[m++] = j;
         sM = m;
     }
+    for (int c = tid; c < k; c += kThreads) sYoff[c] = static_cast<int64_t>(sS[c]) * a.qb * a.s;
+    for (int j = tid; j < k; j += kThreads) {
+        sOoff[j] = static_cast<int64_t>(j) * a.qb * a.ldo;
+        const int64_t lim = a.q - static_cast<int64_t>(j) * a.qb;
+        sLim[j] = static_cast<int32_t>(lim < 0 ? 0 : (lim > a.qb ? a.qb : lim));
+    }
     __syncthreads();
     const int m = sM;
     const int first_par = k - m;          // sorted: systematic survivors first, then parity
 
     if (m > 0) {
-        // sMat[a][bb] = G[S_par[a]][M[bb]];  D[c][a] = right-hand side column c.
+        // sMat[r][cb] = G[S_par[r]][M[cb]];  column c of D starts as column c
+        // of the right-hand side [-G[S_par, S_sys] | I]; rows >= m stay 0.
         for (int e = tid; e < m * m; e += kThreads) {
             const int ra = e / m, cb = e % m;
             sMat[ra * ST + cb] = a.G[static_cast<int64_t>(sS[first_par + ra]) * k + sMiss[cb]];
         }
-        for (int e = tid; e < m * k; e += kThreads) {
-            const int c = e / m, ra = e % m;
-            const int sc = sS[c];
-            double v;
-            if (sc < k)
-                v = -a.G[static_cast<int64_t>(sS[first_par + ra]) * k + sc];
-            else
-                v = (c - first_par == ra) ? 1.0 : 0.0;
+        for (int e = tid; e < ST * k; e += kThreads) {
+            const int c = e / ST, ra = e % ST;
+            double v = 0.0;
+            if (ra < m) {
+                const int sc = sS[c];
+                v = sc < k ? -a.G[static_cast<int64_t>(sS[first_par + ra]) * k + sc]
+                           : ((c - first_par == ra) ? 1.0 : 0.0);
+            }
             sD[c * ST + ra] = v;
         }
         __syncthreads();
@@ -141,8 +200,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
             __syncthreads();
             const int rows = m - j - 1;
             if (rows > 0) {
-                for (int e = tid; e < rows * (m - j - 1); e += kThreads) {
-                    const int i = j + 1 + e / (m - j - 1), c = j + 1 + e % (m - j - 1);
+                for (int e = tid; e < rows * rows; e += kThreads) {
+                    const int i = j + 1 + e / rows, c = j + 1 + e % rows;
                     sMat[i * ST + c] -= sL[i] * sMat[j * ST + c];
                 }
                 for (int e = tid; e < rows * k; e += kThreads) {
@@ -168,73 +227,98 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
     }
     if (writer) a.info[b] = 0;
 
-    // Apply: element e of a block is (row t, column col) with t = e / s.
+    // Apply.
     const YT* Y = static_cast<const YT*>(a.Y);
     float* out = a.out + b * a.out_stride;
-    const int64_t total = a.qb * a.s;
-    const int64_t e0 = chunk * elems_per_block;
-    const int64_t e1 = min(total, e0 + elems_per_block);
-    for (int64_t e = e0 + tid; e < e1; e += kThreads) {
-        const int64_t t = e / a.s, col = e - t * a.s;
-        double acc[MAXM];
+    const int total = static_cast<int>(a.qb * a.s);
+    const int s = static_cast<int>(a.s);
+    const int e0 = static_cast<int>(chunk) * elems_per_block;
+    const int e1 = min(total, e0 + elems_per_block);
+    const int passes = m > 0 ? (m + PASS - 1) / PASS : 1;
+    for (int e = e0 + E * tid; e < e1; e += E * kThreads) {
+        const int t = e / s, col = e - t * s;      // E = 4: the four elements share row t
+        for (int pass = 0; pass < passes; ++pass) {
+            const int p0 = pass * PASS;
+            double acc[PASS][E];
 #pragma unroll
-        for (int bb = 0; bb < MAXM; ++bb) acc[bb] = 0.0;
-        for (int c = 0; c < k; ++c) {
-            const int w = sS[c];
-            const double y = static_cast<double>(Y[(static_cast<int64_t>(w) * a.qb + t) * a.s + col]);
-            if (w < k) {
-                const int64_t row = static_cast<int64_t>(w) * a.qb + t;
-                if (row < a.q) out[row * a.ldo + col] = static_cast<float>(y);
+            for (int bb = 0; bb < PASS; ++bb)
+#pragma unroll
+                for (int v = 0; v < E; ++v) acc[bb][v] = 0.0;
+            for (int c = 0; c < k; ++c) {
+                double y[E];
+                Vec<E, YT>::load(Y + sYoff[c] + e, y);
+                const int w = sS[c];
+                if (pass == 0 && w < k && t < sLim[w]) store_out<E>(out + sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, y);
+                const double* dp = sD + c * ST + p0;
+#pragma unroll
+                for (int bb = 0; bb < PASS; bb += 2) {
+                    if (p0 + bb < m) {
+                        const double2 d = *reinterpret_cast<const double2*>(dp + bb);
+#pragma unroll
+                        for (int v = 0; v < E; ++v) {
+                            acc[bb][v] = fma(d.x, y[v], acc[bb][v]);
+                            acc[bb + 1][v] = fma(d.y, y[v], acc[bb + 1][v]);
+                        }
+                    }
+                }
             }
 #pragma unroll
-            for (int bb = 0; bb < MAXM; ++bb)
-                if (bb < m) acc[bb] = fma(sD[c * ST + bb], y, acc[bb]);
-        }
-#pragma unroll
-        for (int bb = 0; bb < MAXM; ++bb) {
-            if (bb < m) {
-                const int64_t row = static_cast<int64_t>(sMiss[bb]) * a.qb + t;
-                if (row < a.q) out[row * a.ldo + col] = static_cast<float>(acc[bb]);
+            for (int bb = 0; bb < PASS; ++bb) {
+                if (p0 + bb < m) {
+                    const int w = sMiss[p0 + bb];
+                    if (t < sLim[w]) store_out<E>(out + sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, acc[bb]);
+                }
             }
         }
     }
 }
 
-template <int MAXM>
-hipError_t launch_m(const DecodeArgs& a, const DecodeSet& single, int st_rows, hipStream_t st) {
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) % 16) == 0; }
+
+template <int PASS, int E>
+hipError_t launch_pe(const DecodeArgs& a, const DecodeSet& single, int st_rows, hipStream_t st) {
     const int64_t total = a.qb * a.s;
-    const int64_t max_chunks = std::max<int64_t>(1, ceil_div(total, kThreads));
+    // One workgroup per set once the batch fills the chip; a few sets are split
+    // over several workgroups.
+    const int64_t max_chunks = std::max<int64_t>(1, ceil_div(total, static_cast<int64_t>(kThreads) * E));
     const int64_t want = std::max<int64_t>(1, ceil_div(2048, a.batch));
     const int64_t chunks = std::min(max_chunks, want);
-    const int64_t per = ceil_div(std::max<int64_t>(total, 1), chunks);
+    const int64_t per = ceil_div(ceil_div(std::max<int64_t>(total, 1), chunks), E) * E;
     const int64_t blocks = chunks * a.batch;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     const size_t shmem = decode_lds_bytes(a.k, st_rows);
     if (a.y_f64)
-        hipLaunchKernelGGL((decode_kernel<MAXM, double>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), shmem,
-                           st, a, single, chunks, per, st_rows);
+        hipLaunchKernelGGL((decode_kernel<PASS, E, double>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads),
+                           shmem, st, a, single, chunks, static_cast<int>(per), st_rows);
     else
-        hipLaunchKernelGGL((decode_kernel<MAXM, float>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), shmem,
-                           st, a, single, chunks, per, st_rows);
+        hipLaunchKernelGGL((decode_kernel<PASS, E, float>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads),
+                           shmem, st, a, single, chunks, static_cast<int>(per), st_rows);
     return hipGetLastError();
+}
+
+template <int PASS>
+hipError_t launch_p(const DecodeArgs& a, const DecodeSet& single, int st_rows, hipStream_t st) {
+    const bool vec4 = a.s % 4 == 0 && a.ldo % 4 == 0 && aligned16(a.out) && aligned16(a.Y) &&
+                      (a.batch == 1 || a.out_stride % 4 == 0);
+    return vec4 ? launch_pe<PASS, 4>(a, single, st_rows, st) : launch_pe<PASS, 1>(a, single, st_rows, st);
 }
 
 }  // namespace
 
 size_t decode_lds_bytes(int k, int mmax) {
-    return static_cast<size_t>(k * mmax + mmax * mmax) * sizeof(double);
+    const int st = (std::max(mmax, 1) + 1) / 2 * 2;
+    return static_cast<size_t>(k * st + st * st + st) * sizeof(double);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax, hipStream_t st) {
     if (a.batch == 0) return hipSuccess;
+    if (a.qb * a.s > 0x7FFFFFFF) return hipErrorInvalidValue;
     DecodeSet s{};
     if (single) s = *single;
-    const int rows = std::max(mmax, 1);
-    if (mmax <= 4) return launch_m<4>(a, s, rows, st);
-    if (mmax <= 8) return launch_m<8>(a, s, rows, st);
-    if (mmax <= 16) return launch_m<16>(a, s, rows, st);
-    if (mmax <= 32) return launch_m<32>(a, s, rows, st);
-    return launch_m<64>(a, s, rows, st);
+    const int rows = (std::max(mmax, 1) + 1) / 2 * 2;   // even: D pairs are read 16 bytes at a time
+    if (mmax <= 2) return launch_p<2>(a, s, rows, st);
+    if (mmax <= 4) return launch_p<4>(a, s, rows, st);
+    return launch_p<8>(a, s, rows, st);
 }
 
 }  // namespace coded

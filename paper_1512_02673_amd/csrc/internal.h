@@ -54,8 +54,10 @@ hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st);
 hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- decode
+// One survivor set passed by value (worker indices < 128 fit in a byte;
+// packed four to a word so the kernel can pick them out of its arguments).
 struct DecodeSet {
-    int32_t idx[kMaxN];
+    uint32_t packed[kMaxN / 4];
 };
 struct DecodeArgs {
     const double* G;      // device n x k

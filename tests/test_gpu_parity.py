@@ -391,3 +391,40 @@ def test_matmul_empty_and_argument_errors(lib, torch):
     with pytest.raises(ValueError):
         lib.coded_matmul(code, torch.zeros((4, 8), device="cuda"), par, torch.zeros(7, device="cuda"), out, ws, info,
                          1, 0)
+
+
+@pytest.mark.parametrize("s,pad", [(8, 4), (8, 1), (4, 0), (3, 0), (12, 4)])
+def test_decode_many_missing_blocks_and_strided_out(lib, torch, s, pad):
+    """Sets with up to 20 parity survivors (several register passes), outputs with
+    row stride ldo = s + pad, fp64 and fp32 worker results."""
+    n, k, q, r = 48, 24, 500, 16
+    P, A, X = make_inputs(n, k, q, r, s, 16)
+    G = oc.systematic_generator(P)
+    Y = oc.worker_products(oc.encode(G, oc.pad_and_split(A, k)), X)
+    code = lib.Code(n, k, G, 2)
+    rng = np.random.default_rng(3)
+    sets = []
+    for mm in (0, 1, 7, 8, 9, 15, 16, 17, 20, 24):
+        par = rng.choice(np.arange(k, n), size=mm, replace=False)
+        sysw = rng.choice(np.arange(k), size=k - mm, replace=False)
+        sets.append(np.sort(np.concatenate([sysw, par])).astype(np.int32))
+    for ydt in (torch.float64, torch.float32):
+        dY = torch.from_numpy(Y).to("cuda").to(ydt)
+        base = torch.full((len(sets), q, s + pad), float("nan"), dtype=torch.float32, device="cuda")
+        out = base[:, :, :s]
+        info = info_tensor(torch, len(sets))
+        lib.coded_decode_batched(code, torch.from_numpy(np.stack(sets)).cuda(), dY, q, out, info)
+        torch.cuda.synchronize()
+        assert np.all(info.cpu().numpy() == 0)
+        got_all = base.cpu().numpy()
+        for bi, S in enumerate(sets):
+            ref = oc.decode_from_all(G, S, Y, q)
+            tol = (2.0 ** -23 if ydt == torch.float64 else 2.0 ** -20) + 1e-14 * np.linalg.cond(G[S]) * k
+            if ydt == torch.float32:
+                tol += 2.0 ** -23 * np.linalg.cond(G[S]) * k
+            assert normwise_rel_err(got_all[bi, :, :s], ref) <= tol, (bi, ydt)
+            assert np.all(np.isnan(got_all[bi, :, s:]))          # the row padding is never written
+            single = torch.full((q, s + pad), float("nan"), dtype=torch.float32, device="cuda")
+            lib.coded_decode(code, S, dY, q, single[:, :s], info[:1])
+            torch.cuda.synchronize()
+            assert np.array_equal(single.cpu().numpy()[:, :s], got_all[bi, :, :s])

@@ -1,0 +1,95 @@
+"""GPU parity at the workloads' full sizes, in the launch configurations bench.py times.
+
+Every decoded output is checked against the oracle's fp64 product A X (a
+property that holds for every survivor set), sampled ones also against the
+oracle's own coded pipeline, and every survivor set bit for bit against the
+oracle's draw.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import coded as oc
+from tests.gpu_helpers import torch_mod
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-4
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = torch_mod()
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def per_set_errors(torch, out, ref):
+    """Normwise relative error of each decoded set (batch, q, s) against ref (q, s), on the GPU."""
+    den = ref.abs().amax(dim=0)
+    errs = []
+    for b0 in range(0, out.shape[0], 500):
+        d = (out[b0:b0 + 500].double() - ref.unsqueeze(0)).abs().amax(dim=1) / den
+        errs.append(d.amax(dim=1))
+    return torch.cat(errs).cpu().numpy()
+
+
+def test_gemv_workload_full_size(lib, torch):
+    """(16,12) code, A 65536 x 8192 fp32: coded_matmul for several draws with fresh x."""
+    w = synth.WORKLOADS["gemv16x12_65536x8192"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    P = synth.parity_matrix(n, k, seed)
+    code = lib.Code.systematic(P, 2)
+    dA = torch.from_numpy(A).cuda()
+    par = lib.alloc_parity(code, q, r, torch.float32)
+    ws = lib.alloc_y(code, q, 1, torch.float64)
+    out = torch.empty(q, dtype=torch.float32, device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    A64 = A.astype(np.float64)
+    for t in range(4):
+        x = synth.gaussian((r,), seed, synth.STREAM_X, t)
+        surv, T = lib.coded_matmul(code, dA, par, torch.from_numpy(x).cuda(), out, ws, info, seed, t,
+                                   parity_ready=t > 0)
+        torch.cuda.synchronize()
+        S, T_ref = oc.draw_survivors(n, k, seed, t)
+        assert np.array_equal(surv, S) and int(info.item()) == 0
+        ref = oc.plain_product(A64, x)[:, 0]
+        err = float(np.max(np.abs(out.cpu().numpy() - ref)) / np.max(np.abs(ref)))
+        assert err <= TOL_F32, (t, err)
+
+
+def test_decode_heavy_workload_full_size(lib, torch):
+    """(64,48) code, A 16384 x 4096 fp32, X 4096 x 8: all 10000 distinct survivor sets
+    (>= 8 parity survivors each) decoded in one batched launch."""
+    w = synth.WORKLOADS["decode64x48_16384x4096x8"]
+    n, k, q, r, s, seed, B = w.n, w.k, w.q, w.r, w.s, w.seed, w.units
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    X = synth.gaussian((r, s), seed, synth.STREAM_X)
+    P = synth.parity_matrix(n, k, seed)
+    code = lib.Code.systematic(P, 2)
+    dA, dX = torch.from_numpy(A).cuda(), torch.from_numpy(X).cuda()
+    par = lib.alloc_parity(code, q, r, torch.float32)
+    Y = lib.alloc_y(code, q, s, torch.float64)
+    lib.coded_encode(code, dA, par)
+    lib.coded_worker_mm(code, dA, par, dX, Y)
+    sets, nxt = lib.coded_draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
+    sets_ref, nxt_ref = oc.draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
+    assert np.array_equal(sets, sets_ref) and nxt == nxt_ref
+    out = torch.full((B, q, s), float("nan"), dtype=torch.float32, device="cuda")
+    info = torch.full((B,), 7, dtype=torch.int32, device="cuda")
+    lib.coded_decode_batched(code, torch.from_numpy(sets).cuda(), Y, q, out, info)
+    torch.cuda.synchronize()
+    assert int((info != 0).sum().item()) == 0
+    ref = torch.from_numpy(oc.plain_product(A, X)).cuda()
+    errs = per_set_errors(torch, out, ref)
+    assert np.all(np.isfinite(errs)) and float(errs.max()) <= TOL_F32, float(errs.max())
+    # sampled sets against the oracle's own encode / worker products / LU decode
+    G = oc.systematic_generator(P)
+    Yo = oc.worker_products(oc.encode(G, oc.pad_and_split(A, k)), X)
+    for b in np.linspace(0, B - 1, 12).astype(int):
+        ref_b = oc.decode_from_all(G, sets[b], Yo, q)
+        got = out[b].cpu().numpy().astype(np.float64)
+        den = np.max(np.abs(ref_b), axis=0)
+        assert float(np.max(np.max(np.abs(got - ref_b), axis=0) / den)) <= TOL_F32
