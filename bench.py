@@ -285,6 +285,85 @@ def cpu_baseline_decode(w, A, X, P, sets, out_dev, count):
             "gpu_vs_oracle_max_rel_err": worst}
 
 
+def gd_workload(args):
+    """Coded gradient descent for least squares (Sec. III-E): A 262144 x 4096 fp32
+    N(0, 1/4096), y = A w* + N(0, 0.01) noise, (20,16) codes for A and for A^T,
+    step 0.5 normalised by q * sigma^2 = 64.  One step = one iteration (two coded
+    products, residual and update fused into the decodes)."""
+    import torch
+
+    from paper_1512_02673_amd import binding as lib
+
+    w = synth.WORKLOADS["gd20x16_262144x4096"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    K, W = args.steps, args.warmup
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A, std=w.a_std)
+    wstar = synth.gaussian((r,), seed, synth.STREAM_WSTAR)
+    noise = synth.gaussian((q,), seed, synth.STREAM_NOISE)
+    cA = lib.Code.systematic(synth.parity_matrix(n, k, seed), 2)
+    cT = lib.Code.systematic(synth.parity_matrix(n, k, seed, synth.STREAM_PT), 2)
+    dA = torch.from_numpy(A).cuda()
+    # y = A w* + noise, formed once on the device in fp64 as input preparation
+    dy = (dA.double() @ torch.from_numpy(wstar).cuda().double() +
+          w.extra["noise_std"] * torch.from_numpy(noise).cuda().double()).float()
+    eta = w.extra["eta"] / (q * w.a_std ** 2)
+    dAT = torch.empty((r, q), dtype=torch.float32, device="cuda")
+    lib.coded_transpose(dA, dAT)
+    pA, pT = lib.alloc_parity(cA, q, r, torch.float32), lib.alloc_parity(cT, r, q, torch.float32)
+    lib.coded_encode(cA, dA, pA)
+    lib.coded_encode(cT, dAT, pT)
+    x = torch.zeros(r, dtype=torch.float32, device="cuda")
+    ws = torch.empty(lib.coded_gd_sizes(cA, cT, q, r), dtype=torch.uint8, device="cuda")
+    info = torch.zeros(2, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for t in range(W):
+        lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, t, ws, info)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    start = time.perf_counter()
+    for i in range(K):
+        evs[i][0].record(stream)
+        lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, W + i, ws, info)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - start
+    if int(info.abs().sum().item()) != 0:
+        raise RuntimeError("a decode reported a singular or invalid survivor set")
+    step_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    # The two worker GEMV launches of a step, timed alone on the same buffers.
+    Y1 = lib.alloc_y(cA, q, 1, torch.float64)
+    Y2 = lib.alloc_y(cT, r, 1, torch.float64)
+    z = torch.zeros(q, dtype=torch.float32, device="cuda")
+    g = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(40)]
+    for i in range(20):
+        g[2 * i][0].record(stream)
+        lib.coded_worker_mm(cA, dA, pA, x, Y1)
+        g[2 * i][1].record(stream)
+        g[2 * i + 1][0].record(stream)
+        lib.coded_worker_mm(cT, dAT, pT, z, Y2)
+        g[2 * i + 1][1].record(stream)
+    torch.cuda.synchronize()
+    tA = float(np.mean([g[2 * i][0].elapsed_time(g[2 * i][1]) for i in range(20)]))
+    tT = float(np.mean([g[2 * i + 1][0].elapsed_time(g[2 * i + 1][1]) for i in range(20)]))
+    qbA, qbT = cA.qb(q), cT.qb(r)
+    bA = 4.0 * q * r + 4.0 * 2 * (n - k) * qbA * r + 4.0 * r + 8.0 * n * qbA
+    bT = 4.0 * r * q + 4.0 * 2 * (n - k) * qbT * q + 4.0 * q + 8.0 * n * qbT
+    achieved = (bA + bT) / ((tA + tT) * 1e-3) / 1e9
+    result = {
+        "metric": METRIC, "value": K / elapsed, "unit": "iterations/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "eta_applied": eta,
+                   "codes": "separate (20,16) systematic codes for A and A^T, hi+lo parity"},
+        "step_ms_events": step_ms, "gemv_A_ms": tA, "gemv_AT_ms": tT,
+        "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel (A and A^T launches)", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "algorithmic_bytes_per_launch": [bA, bT], "traffic": None,
+                     "step_frac": (bA + bT) / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+    }
+    return result
+
+
 def calibrate_copy(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -302,7 +381,7 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
-                    choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8"])
+                    choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8", "gd20x16_262144x4096"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-products", type=int, default=300)
     ap.add_argument("--cpu-decodes", type=int, default=1000)
@@ -327,6 +406,12 @@ def main():
         if "--warmup" not in sys.argv:
             args.warmup = 3
         result = decode_workload(args)
+    elif args.workload == "gd20x16_262144x4096":
+        if "--steps" not in sys.argv:
+            args.steps = 200
+        if "--warmup" not in sys.argv:
+            args.warmup = 5
+        result = gd_workload(args)
     else:
         result = gemv_workload(args)
     print(json.dumps(result), flush=True)

@@ -207,6 +207,47 @@ coded_status coded_matmul(const coded_code* code, coded_dtype dt, const void* A,
                           uint64_t draw, double shift, double rate, int32_t* survivors_out, double* t_overall_out,
                           float* out, int64_t ldo, void* workspace, int32_t* info, void* stream);
 
+/*
+ * coded_transpose -- AT = A^T for fp32 A (q x r, row stride lda) into AT
+ * (r x q, row stride ldat >= q).  This forms the column split of A that the
+ * transposed code of coded gradient descent encodes (Sec. III-E: worker i
+ * stores the i-th row split of A and the i-th column split).  Device
+ * pointers; A and AT must not overlap.
+ */
+coded_status coded_transpose(const float* A, int64_t q, int64_t r, int64_t lda, float* AT, int64_t ldat,
+                             void* stream);
+
+/*
+ * coded_gd_sizes -- workspace bytes of coded_gd_step for codes codeA (over
+ * the q rows of A) and codeAT (over the r rows of A^T).
+ */
+coded_status coded_gd_sizes(const coded_code* codeA, const coded_code* codeAT, int64_t q, int64_t r,
+                            int64_t* workspace_bytes);
+
+/*
+ * coded_gd_step -- one iteration of coded gradient descent for least squares
+ * (Sec. III-E, eq. exact_gradient): x <- x - eta * A^T (A x - y), where A x is
+ * an (n1,k1)-coded product over the row split of A (code codeA, survivors of
+ * draw 2*iteration) and A^T z an (n2,k2)-coded product over the row split of
+ * A^T (code codeAT, survivors of draw 2*iteration + 1).  The residual
+ * z = A x - y and the update are fused into the two decodes.
+ *   A, parityA    device fp32, q x r (row stride lda) and its coded parity
+ *                 (coded_encode with codeA).
+ *   AT, parityAT  device fp32, r x q (row stride ldat; e.g. from
+ *                 coded_transpose) and its coded parity (codeAT).
+ *   y             device fp32[q]; x device fp32[r], updated in place.
+ *   eta           step size as applied (no normalisation inside).
+ *   workspace     device, coded_gd_sizes bytes (worker results of both
+ *                 products and z).
+ *   info          device int32[2]: decode status of the two products.
+ *   survivors_out host int32[k1 + k2] or NULL: both survivor sets, ascending.
+ */
+coded_status coded_gd_step(const coded_code* codeA, const coded_code* codeAT, const float* A, int64_t lda,
+                           const float* parityA, const float* AT, int64_t ldat, const float* parityAT, int64_t q,
+                           int64_t r, const float* y, float* x, double eta, uint64_t seed, uint64_t iteration,
+                           double shift, double rate, void* workspace, int32_t* info, int32_t* survivors_out,
+                           void* stream);
+
 /* Static text of a status code. */
 const char* coded_status_string(coded_status status);
 /* Message of the last failing call on this thread ("" if none). */

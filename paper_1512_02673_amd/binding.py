@@ -39,6 +39,10 @@ _SIGNATURES = {
     "coded_draw_survivor_sets": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_i32, _c_i32, _c_p, _c_p]),
     "coded_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i32, _c_p, _c_i64, _c_i64,
                               _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_transpose": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i64, _c_p]),
+    "coded_gd_sizes": (_c_i32, [_c_p, _c_p, _c_i64, _c_i64, _c_p]),
+    "coded_gd_step": (_c_i32, [_c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_dbl,
+                               _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_p]),
     "coded_status_string": (ctypes.c_char_p, [_c_i32]),
     "coded_last_error": (ctypes.c_char_p, []),
     "coded_version": (ctypes.c_char_p, []),
@@ -238,6 +242,32 @@ def coded_matmul(code: Code, A, parity, X, out, workspace, info, seed: int, draw
                               _ptr(X), s, ldx, seed, draw, shift, rate, surv.ctypes.data_as(ctypes.c_void_p),
                               ctypes.addressof(t), _ptr(out), ldo, _ptr(workspace), _ptr(info), _stream(stream)))
     return surv, t.value
+
+
+def coded_transpose(A, AT, stream=None) -> None:
+    q, r, lda = _matrix(A, "A")
+    r2, q2, ldat = _matrix(AT, "AT")
+    if (r2, q2) != (r, q):
+        raise ValueError("AT must be r x q")
+    _check(lib().coded_transpose(_ptr(A), q, r, lda, _ptr(AT), ldat, _stream(stream)))
+
+
+def coded_gd_sizes(codeA: Code, codeAT: Code, q: int, r: int) -> int:
+    wb = ctypes.c_int64()
+    _check(lib().coded_gd_sizes(codeA.handle, codeAT.handle, q, r, ctypes.addressof(wb)))
+    return wb.value
+
+
+def coded_gd_step(codeA: Code, codeAT: Code, A, parityA, AT, parityAT, y, x, eta: float, seed: int, iteration: int,
+                  workspace, info, shift: float = 1.0, rate: float = 1.0, stream=None):
+    """One coded gradient-descent iteration (x updated in place); returns both survivor sets."""
+    q, r, lda = _matrix(A, "A")
+    _, _, ldat = _matrix(AT, "AT")
+    surv = np.zeros(codeA.k + codeAT.k, dtype=np.int32)
+    _check(lib().coded_gd_step(codeA.handle, codeAT.handle, _ptr(A), lda, _ptr(parityA), _ptr(AT), ldat,
+                               _ptr(parityAT), q, r, _ptr(y), _ptr(x), eta, seed, iteration, shift, rate,
+                               _ptr(workspace), _ptr(info), surv.ctypes.data_as(ctypes.c_void_p), _stream(stream)))
+    return surv[:codeA.k], surv[codeA.k:]
 
 
 # ---------------------------------------------------------------- buffer helpers

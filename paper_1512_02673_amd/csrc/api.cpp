@@ -166,7 +166,8 @@ coded_status take_survivors(const coded_code* c, const int32_t* survivors, int32
 }
 
 coded_status do_decode_single(const coded_code* c, const DecodeSet& set, int m, const void* Y, coded_dtype y_dt,
-                              int64_t q, int64_t s, float* out, int64_t ldo, int32_t* info, hipStream_t st) {
+                              int64_t q, int64_t s, float* out, int64_t ldo, int32_t* info, hipStream_t st,
+                              const float* cvec = nullptr, double alpha = 1.0, double beta = 0.0) {
     if (y_dt != CODED_F64 && y_dt != CODED_F32) return fail(CODED_ERR_ARG, "y_dt must be CODED_F64 or CODED_F32");
     if (q < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q and s must be >= 0");
     if (ldo < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldo must be >= max(s, 1)");
@@ -176,6 +177,9 @@ coded_status do_decode_single(const coded_code* c, const DecodeSet& set, int m, 
     if (decode_lds_bytes(c->k, std::max(m, 1)) > kMaxDecodeLds)
         return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
     DecodeArgs a{c->dG, Y, out, info, nullptr, q, qb, s, ldo, 0, c->n, c->k, 1, y_dt == CODED_F64};
+    a.c = cvec;
+    a.alpha = alpha;
+    a.beta = beta;
     hipError_t e = launch_decode(a, &set, m, st);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     return CODED_OK;
@@ -387,6 +391,76 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     if (coded_status s2 = do_decode_single(c, set, m, workspace, y_dt, q, s, out, ldo, info, st)) return s2;
     if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
     if (t_overall_out) *t_overall_out = t;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_transpose(const float* A, int64_t q, int64_t r, int64_t lda, float* AT, int64_t ldat,
+                             void* stream) {
+    CODED_GUARD_BEGIN
+    if (q < 0 || r < 0) return fail(CODED_ERR_SHAPE, "q and r must be >= 0");
+    if (lda < std::max<int64_t>(r, 1) || ldat < std::max<int64_t>(q, 1)) return fail(CODED_ERR_SHAPE, "bad lda / ldat");
+    if (q > 0 && r > 0 && (!A || !AT)) return fail(CODED_ERR_ARG, "A or AT is NULL");
+    hipError_t e = launch_transpose_f32(A, q, r, lda, AT, ldat, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "transpose launch");
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+namespace {
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+}  // namespace
+
+coded_status coded_gd_sizes(const coded_code* cA, const coded_code* cT, int64_t q, int64_t r,
+                            int64_t* workspace_bytes) {
+    if (!cA || !cT) return fail(CODED_ERR_ARG, "code is NULL");
+    if (q < 0 || r < 0) return fail(CODED_ERR_SHAPE, "q and r must be >= 0");
+    const int64_t y1 = static_cast<int64_t>(cA->n) * block_rows(q, cA->k) * 8;
+    const int64_t y2 = static_cast<int64_t>(cT->n) * block_rows(r, cT->k) * 8;
+    if (workspace_bytes) *workspace_bytes = align256(y1) + align256(y2) + align256(q * 4);
+    return CODED_OK;
+}
+
+coded_status coded_gd_step(const coded_code* cA, const coded_code* cT, const float* A, int64_t lda,
+                           const float* parityA, const float* AT, int64_t ldat, const float* parityAT, int64_t q,
+                           int64_t r, const float* y, float* x, double eta, uint64_t seed, uint64_t iteration,
+                           double shift, double rate, void* workspace, int32_t* info, int32_t* survivors_out,
+                           void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(cA)) return st;
+    if (coded_status st = check_code(cT)) return st;
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    if (coded_status st = check_ar(r, q, ldat)) return st;
+    if (q == 0 || r == 0) return fail(CODED_ERR_SHAPE, "q and r must be > 0");
+    if (!y || !x || !workspace || !info) return fail(CODED_ERR_ARG, "y, x, workspace or info is NULL");
+    if (!(rate > 0.0) || !std::isfinite(shift) || !std::isfinite(eta)) return fail(CODED_ERR_ARG, "need rate > 0, finite shift and eta");
+    if (iteration >= (1ull << 38)) return fail(CODED_ERR_ARG, "iteration must be < 2^38");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // Survivors of both products first (host only; nothing is enqueued on failure).
+    int32_t s1[CODED_MAX_N], s2[CODED_MAX_N];
+    coded_rng::draw_survivors(cA->n, cA->k, seed, 2 * iteration, shift, rate, s1);
+    coded_rng::draw_survivors(cT->n, cT->k, seed, 2 * iteration + 1, shift, rate, s2);
+    DecodeSet set1, set2;
+    int m1 = 0, m2 = 0;
+    if (coded_status e = take_survivors(cA, s1, cA->k, set1, m1)) return e;
+    if (coded_status e = take_survivors(cT, s2, cT->k, set2, m2)) return e;
+    if (decode_lds_bytes(cA->k, std::max(m1, 1)) > kMaxDecodeLds || decode_lds_bytes(cT->k, std::max(m2, 1)) > kMaxDecodeLds)
+        return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
+    char* ws = static_cast<char*>(workspace);
+    double* Y1 = reinterpret_cast<double*>(ws);
+    double* Y2 = reinterpret_cast<double*>(ws + align256(static_cast<int64_t>(cA->n) * block_rows(q, cA->k) * 8));
+    float* z = reinterpret_cast<float*>(reinterpret_cast<char*>(Y2) +
+                                        align256(static_cast<int64_t>(cT->n) * block_rows(r, cT->k) * 8));
+    // z = A x - y  (coded product with code A, residual fused into the decode)
+    if (coded_status e = do_workers(cA, CODED_F32, A, q, r, lda, parityA, x, 1, 1, nullptr, Y1, CODED_F64, st)) return e;
+    if (coded_status e = do_decode_single(cA, set1, m1, Y1, CODED_F64, q, 1, z, 1, info, st, y, 1.0, -1.0)) return e;
+    // x = x - eta A^T z  (coded product with the code of A^T, update fused into the decode)
+    if (coded_status e = do_workers(cT, CODED_F32, AT, r, q, ldat, parityAT, z, 1, 1, nullptr, Y2, CODED_F64, st)) return e;
+    if (coded_status e = do_decode_single(cT, set2, m2, Y2, CODED_F64, r, 1, x, 1, info + 1, st, x, -eta, 1.0)) return e;
+    if (survivors_out) {
+        std::copy(s1, s1 + cA->k, survivors_out);
+        std::copy(s2, s2 + cT->k, survivors_out + cA->k);
+    }
     return CODED_OK;
     CODED_GUARD_END
 }

@@ -66,13 +66,29 @@ struct Vec<4, float> {
     }
 };
 
+// out = v, or alpha * v + beta * c when an epilogue operand is given (c has
+// out's layout; the element is read before it is written, so c may be out).
 template <int E>
-__device__ inline void store_out(float* p, const double* v) {
+__device__ inline void store_out(const DecodeArgs& a, float* p, int64_t off, const double* v) {
+    double w[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) w[i] = v[i];
+    if (a.c) {
+        float cv[E];
+        if constexpr (E == 4) {
+            const float4 f = *reinterpret_cast<const float4*>(a.c + off);
+            cv[0] = f.x; cv[1] = f.y; cv[2] = f.z; cv[3] = f.w;
+        } else {
+            cv[0] = a.c[off];
+        }
+#pragma unroll
+        for (int i = 0; i < E; ++i) w[i] = fma(a.alpha, w[i], a.beta * static_cast<double>(cv[i]));
+    }
     if constexpr (E == 4)
-        *reinterpret_cast<float4*>(p) = make_float4(static_cast<float>(v[0]), static_cast<float>(v[1]),
-                                                    static_cast<float>(v[2]), static_cast<float>(v[3]));
+        *reinterpret_cast<float4*>(p + off) = make_float4(static_cast<float>(w[0]), static_cast<float>(w[1]),
+                                                          static_cast<float>(w[2]), static_cast<float>(w[3]));
     else
-        p[0] = static_cast<float>(v[0]);
+        p[off] = static_cast<float>(w[0]);
 }
 
 // PASS: missing outputs computed per sweep over the survivors (register
@@ -248,7 +264,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
                 double y[E];
                 Vec<E, YT>::load(Y + sYoff[c] + e, y);
                 const int w = sS[c];
-                if (pass == 0 && w < k && t < sLim[w]) store_out<E>(out + sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, y);
+                if (pass == 0 && w < k && t < sLim[w]) store_out<E>(a, out, sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, y);
                 const double* dp = sD + c * ST + p0;
 #pragma unroll
                 for (int bb = 0; bb < PASS; bb += 2) {
@@ -266,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
             for (int bb = 0; bb < PASS; ++bb) {
                 if (p0 + bb < m) {
                     const int w = sMiss[p0 + bb];
-                    if (t < sLim[w]) store_out<E>(out + sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, acc[bb]);
+                    if (t < sLim[w]) store_out<E>(a, out, sOoff[w] + static_cast<int64_t>(t) * a.ldo + col, acc[bb]);
                 }
             }
         }
@@ -299,7 +315,7 @@ hipError_t launch_pe(const DecodeArgs& a, const DecodeSet& single, int st_rows, 
 template <int PASS>
 hipError_t launch_p(const DecodeArgs& a, const DecodeSet& single, int st_rows, hipStream_t st) {
     const bool vec4 = a.s % 4 == 0 && a.ldo % 4 == 0 && aligned16(a.out) && aligned16(a.Y) &&
-                      (a.batch == 1 || a.out_stride % 4 == 0);
+                      (a.batch == 1 || a.out_stride % 4 == 0) && (a.c == nullptr || aligned16(a.c));
     return vec4 ? launch_pe<PASS, 4>(a, single, st_rows, st) : launch_pe<PASS, 1>(a, single, st_rows, st);
 }
 

@@ -67,11 +67,19 @@ struct DecodeArgs {
     const int32_t* sets;  // device batch x k, or null when `single` is used
     int64_t q, qb, s, ldo, out_stride;
     int32_t n, k, batch, y_f64;
+    // Epilogue: out = alpha * decoded + beta * c (c: same layout as out, or
+    // null for out = decoded).  c may alias out.
+    const float* c = nullptr;
+    double alpha = 1.0, beta = 0.0;
 };
 // LDS bytes of the decode kernel's matrices for k survivors and at most mmax
 // missing blocks; launch_decode sizes its dynamic LDS with it.
 size_t decode_lds_bytes(int k, int mmax);
 hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax, hipStream_t st);
+
+// ---------------------------------------------------------------- transpose
+hipError_t launch_transpose_f32(const float* A, int64_t q, int64_t r, int64_t lda, float* AT, int64_t ldat,
+                                hipStream_t st);
 
 }  // namespace coded
 

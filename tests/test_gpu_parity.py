@@ -428,3 +428,48 @@ def test_decode_many_missing_blocks_and_strided_out(lib, torch, s, pad):
             lib.coded_decode(code, S, dY, q, single[:, :s], info[:1])
             torch.cuda.synchronize()
             assert np.array_equal(single.cpu().numpy()[:, :s], got_all[bi, :, :s])
+
+
+@pytest.mark.parametrize("q,r", [(1, 1), (63, 65), (128, 64), (300, 17)])
+def test_transpose_exact(lib, torch, q, r):
+    A = synth.gaussian((q, r), 17, synth.STREAM_A)
+    dA = torch.from_numpy(A).cuda()
+    AT = torch.full((r, q), float("nan"), dtype=torch.float32, device="cuda")
+    lib.coded_transpose(dA, AT)
+    torch.cuda.synchronize()
+    assert np.array_equal(AT.cpu().numpy(), A.T)
+
+
+@pytest.mark.parametrize("q,r,n1,k1,n2,k2", [(4001, 96, 20, 16, 20, 16), (700, 50, 6, 4, 7, 5)])
+def test_coded_gd_matches_oracle_iterates(lib, torch, q, r, n1, k1, n2, k2):
+    """Coded gradient descent (Sec. III-E): every iterate against the oracle's coded_gd."""
+    seed = 18
+    A = synth.gaussian((q, r), seed, synth.STREAM_A, std=1.0 / np.sqrt(r))
+    w = synth.gaussian((r,), seed, synth.STREAM_WSTAR)
+    y = (oc.plain_product(A, w)[:, 0] + 0.1 * synth.gaussian((q,), seed, synth.STREAM_NOISE)).astype(np.float32)
+    P1 = synth.parity_matrix(n1, k1, seed)
+    P2 = synth.parity_matrix(n2, k2, seed, synth.STREAM_PT)
+    eta = 0.5 * r / q                      # step normalised by the mean Hessian scale q * sigma^2
+    iters = 25
+    rec = []
+    oc.coded_gd(A, y, np.zeros(r), oc.systematic_generator(P1), oc.systematic_generator(P2), eta, iters, seed,
+                record=rec)
+    cA, cT = lib.Code.systematic(P1, 2), lib.Code.systematic(P2, 2)
+    dA = torch.from_numpy(A).cuda()
+    dAT = torch.empty((r, q), dtype=torch.float32, device="cuda")
+    lib.coded_transpose(dA, dAT)
+    pA, pT = lib.alloc_parity(cA, q, r, torch.float32), lib.alloc_parity(cT, r, q, torch.float32)
+    lib.coded_encode(cA, dA, pA)
+    lib.coded_encode(cT, dAT, pT)
+    dy = torch.from_numpy(y).cuda()
+    x = torch.zeros(r, dtype=torch.float32, device="cuda")
+    ws = torch.empty(lib.coded_gd_sizes(cA, cT, q, r), dtype=torch.uint8, device="cuda")
+    info = torch.full((2,), 9, dtype=torch.int32, device="cuda")
+    for t in range(iters):
+        S1, S2 = lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, t, ws, info)
+        assert np.array_equal(S1, oc.draw_survivors(n1, k1, seed, 2 * t)[0])
+        assert np.array_equal(S2, oc.draw_survivors(n2, k2, seed, 2 * t + 1)[0])
+        torch.cuda.synchronize()
+        assert np.all(info.cpu().numpy() == 0)
+        xt = x.cpu().numpy().astype(np.float64)
+        assert np.max(np.abs(xt - rec[t])) <= 1e-4 * np.max(np.abs(rec[t])), t

@@ -93,3 +93,45 @@ def test_decode_heavy_workload_full_size(lib, torch):
         got = out[b].cpu().numpy().astype(np.float64)
         den = np.max(np.abs(ref_b), axis=0)
         assert float(np.max(np.max(np.abs(got - ref_b), axis=0) / den)) <= TOL_F32
+
+
+def test_gd_workload_full_size(lib, torch):
+    """(20,16) codes for A (262144 x 4096, N(0, 1/4096)) and A^T: sampled iterations against the plain
+    fp64 update of the same iterate, survivors against the oracle, and first-order optimality after
+    the 200 iterations of the workload."""
+    w = synth.WORKLOADS["gd20x16_262144x4096"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A, std=w.a_std)
+    wstar = synth.gaussian((r,), seed, synth.STREAM_WSTAR)
+    A64 = A.astype(np.float64)
+    y = (A64 @ wstar.astype(np.float64) + w.extra["noise_std"] * synth.gaussian((q,), seed, synth.STREAM_NOISE)
+         ).astype(np.float32)
+    eta = w.extra["eta"] / (q * w.a_std ** 2)
+    cA = lib.Code.systematic(synth.parity_matrix(n, k, seed), 2)
+    cT = lib.Code.systematic(synth.parity_matrix(n, k, seed, synth.STREAM_PT), 2)
+    dA = torch.from_numpy(A).cuda()
+    dAT = torch.empty((r, q), dtype=torch.float32, device="cuda")
+    lib.coded_transpose(dA, dAT)
+    pA, pT = lib.alloc_parity(cA, q, r, torch.float32), lib.alloc_parity(cT, r, q, torch.float32)
+    lib.coded_encode(cA, dA, pA)
+    lib.coded_encode(cT, dAT, pT)
+    dy = torch.from_numpy(y).cuda()
+    x = torch.zeros(r, dtype=torch.float32, device="cuda")
+    ws = torch.empty(lib.coded_gd_sizes(cA, cT, q, r), dtype=torch.uint8, device="cuda")
+    info = torch.zeros(2, dtype=torch.int32, device="cuda")
+    y64 = y.astype(np.float64)
+    for t in range(w.units):
+        before = x.cpu().numpy().astype(np.float64) if t in (0, 1, 7, 199) else None
+        S1, S2 = lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, t, ws, info)
+        if before is not None:
+            torch.cuda.synchronize()
+            assert np.array_equal(S1, oc.draw_survivors(n, k, seed, 2 * t)[0])
+            assert np.array_equal(S2, oc.draw_survivors(n, k, seed, 2 * t + 1)[0])
+            assert np.all(info.cpu().numpy() == 0)
+            want = before - eta * (A64.T @ (A64 @ before - y64))
+            got = x.cpu().numpy().astype(np.float64)
+            assert np.max(np.abs(got - want)) <= 1e-4 * np.max(np.abs(want)), t
+    torch.cuda.synchronize()
+    xf = x.cpu().numpy().astype(np.float64)
+    grad = A64.T @ (A64 @ xf - y64)
+    assert np.linalg.norm(grad) <= 1e-4 * np.linalg.norm(A64.T @ y64)
