@@ -97,11 +97,17 @@ coded_status coded_code_info(const coded_code* code, int32_t* n, int32_t* k, int
  *   parity_bytes     the parity buffer (planes * (n-k) * qb * r elements of dt)
  *   y_bytes          Y (n * qb * s elements of y_dt)
  *   workspace_bytes  workspace of coded_matmul (its Y, in y_dt = F64 for F32
- *                    inputs and F32 for BF16 inputs)
+ *                    inputs and F32 for BF16 inputs, followed by the worker
+ *                    workspace)
+ *   worker_workspace_bytes  workspace of coded_worker_mm: 0 for F32 inputs;
+ *                    X transposed (s x r bf16, 256-byte aligned size) for
+ *                    BF16 inputs, so that the matrix-core kernel reads X
+ *                    along K in 16-byte pieces
  * Any output pointer may be NULL.
  */
 coded_status coded_sizes(const coded_code* code, coded_dtype dt, coded_dtype y_dt, int64_t q, int64_t r,
-                         int64_t s, int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes);
+                         int64_t s, int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes,
+                         int64_t* worker_workspace_bytes);
 
 /*
  * coded_encode -- the n-k parity blocks A'_{k+p} = sum_j P[p][j] A_j
@@ -127,11 +133,14 @@ coded_status coded_encode(const coded_code* code, coded_dtype dt, const void* A,
  *   Y          device, n x qb x s of y_dt (layout above).
  *   y_dt       CODED_F64 (dt = F32: products accumulate in fp64) or
  *              CODED_F32 (dt = F32: fp64 accumulate, rounded on store;
- *              dt = BF16: fp32 accumulate).
+ *              dt = BF16: fp32 accumulate on the matrix cores).
+ *   workspace  device, coded_sizes' worker_workspace_bytes; may be NULL when
+ *              that size is 0 (fp32 inputs).  For bf16 inputs NULL selects a
+ *              slower vector kernel.
  */
 coded_status coded_worker_mm(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                              const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* worker_mask,
-                             void* Y, coded_dtype y_dt, void* stream);
+                             void* Y, coded_dtype y_dt, void* workspace, void* stream);
 
 /*
  * coded_decode -- dec(indices, results) of Sec. III-A for one survivor set.

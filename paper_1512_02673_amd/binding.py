@@ -28,10 +28,10 @@ _SIGNATURES = {
     "coded_code_create": (_c_i32, [_c_i32, _c_i32, _c_p, _c_i32, ctypes.POINTER(_c_p)]),
     "coded_code_destroy": (_c_i32, [_c_p]),
     "coded_code_info": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
-    "coded_sizes": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_sizes": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]),
     "coded_encode": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p]),
     "coded_worker_mm": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_p,
-                                 _c_p, _c_i32, _c_p]),
+                                 _c_p, _c_i32, _c_p, _c_p]),
     "coded_decode": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p]),
     "coded_decode_batched": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i64,
                                       _c_p, _c_p]),
@@ -184,10 +184,11 @@ class Code:
 
 
 def coded_sizes(code: Code, dt: int, y_dt: int, q: int, r: int, s: int):
-    pb, yb, wb = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    """(parity_bytes, y_bytes, matmul workspace_bytes, worker workspace_bytes)."""
+    pb, yb, wb, ww = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     _check(lib().coded_sizes(code.handle, dt, y_dt, q, r, s, ctypes.addressof(pb), ctypes.addressof(yb),
-                             ctypes.addressof(wb)))
-    return pb.value, yb.value, wb.value
+                             ctypes.addressof(wb), ctypes.addressof(ww)))
+    return pb.value, yb.value, wb.value, ww.value
 
 
 def coded_encode(code: Code, A, parity, stream=None) -> None:
@@ -195,7 +196,29 @@ def coded_encode(code: Code, A, parity, stream=None) -> None:
     _check(lib().coded_encode(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _stream(stream)))
 
 
-def coded_worker_mm(code: Code, A, parity, X, Y, worker_mask=None, stream=None) -> None:
+def worker_workspace(code: Code, A, X):
+    """A device buffer of the worker workspace size for these operands (None if 0 bytes)."""
+    torch = _torch()
+    q, r, _ = _matrix(A, "A")
+    _, s, _ = _matrix(X, "X")
+    y_dt = CODED_F32 if _dtype_code(A) == CODED_BF16 else CODED_F64
+    nbytes = coded_sizes(code, _dtype_code(A), y_dt, q, r, s)[3]
+    return torch.empty(nbytes, dtype=torch.uint8, device=A.device) if nbytes else None
+
+
+def matmul_workspace(code: Code, A, X):
+    """A device buffer of coded_matmul's workspace size for these operands."""
+    torch = _torch()
+    q, r, _ = _matrix(A, "A")
+    _, s, _ = _matrix(X, "X")
+    y_dt = CODED_F32 if _dtype_code(A) == CODED_BF16 else CODED_F64
+    nbytes = coded_sizes(code, _dtype_code(A), y_dt, q, r, s)[2]
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=A.device)
+
+
+def coded_worker_mm(code: Code, A, parity, X, Y, worker_mask=None, workspace="auto", stream=None) -> None:
+    """workspace: a device buffer of coded_sizes' worker workspace bytes, None (bf16: vector
+    kernel), or "auto" (allocated here when needed)."""
     q, r, lda = _matrix(A, "A")
     rx, s, ldx = _matrix(X, "X")
     if rx != r:
@@ -206,8 +229,10 @@ def coded_worker_mm(code: Code, A, parity, X, Y, worker_mask=None, stream=None) 
         if m.shape != (code.n,):
             raise ValueError("worker_mask must have n entries")
         mask = m.ctypes.data_as(ctypes.c_void_p)
+    if isinstance(workspace, str):
+        workspace = worker_workspace(code, A, X)
     _check(lib().coded_worker_mm(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _ptr(X), s, ldx,
-                                 mask, _ptr(Y), _dtype_code(Y), _stream(stream)))
+                                 mask, _ptr(Y), _dtype_code(Y), _ptr(workspace), _stream(stream)))
 
 
 def coded_decode(code: Code, survivors, Y, q: int, out, info, stream=None) -> None:

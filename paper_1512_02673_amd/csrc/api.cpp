@@ -52,6 +52,13 @@ coded_status check_code(const coded_code* c) {
 
 int64_t block_rows(int64_t q, int k) { return (q + k - 1) / k; }
 
+// coded_matmul's workspace: its worker results Y (fp64 for fp32 inputs, fp32
+// for bf16), 256-byte aligned, then the worker workspace.
+int64_t matmul_y_bytes(const coded_code* c, coded_dtype dt, int64_t q, int64_t s) {
+    const int64_t b = static_cast<int64_t>(c->n) * block_rows(q, c->k) * s * (dt == CODED_F32 ? 8 : 4);
+    return (b + 255) / 256 * 256;
+}
+
 size_t dtype_size(coded_dtype d) {
     switch (d) {
         case CODED_F32: return 4;
@@ -104,7 +111,7 @@ coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64
 
 coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                         const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* mask, void* Y,
-                        coded_dtype y_dt, hipStream_t st) {
+                        coded_dtype y_dt, void* workspace, hipStream_t st) {
     if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
     if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
     if (s == 1 && ldx != 1 && dt == CODED_F32) {
@@ -134,6 +141,7 @@ coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int6
     a.k = c->k;
     a.planes = c->planes;
     a.y_f64 = y_dt == CODED_F64;
+    a.xt = dt == CODED_BF16 ? workspace : nullptr;
     for (int i = 0; i < c->n; ++i) {
         if (mask && !mask[i]) continue;
         if (i < c->k)
@@ -243,7 +251,8 @@ coded_status coded_code_info(const coded_code* c, int32_t* n, int32_t* k, int32_
 }
 
 coded_status coded_sizes(const coded_code* c, coded_dtype dt, coded_dtype y_dt, int64_t q, int64_t r, int64_t s,
-                         int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes) {
+                         int64_t* parity_bytes, int64_t* y_bytes, int64_t* workspace_bytes,
+                         int64_t* worker_workspace_bytes) {
     CODED_GUARD_BEGIN
     if (!c) return fail(CODED_ERR_ARG, "code is NULL");
     if (coded_status st = check_dt(dt, y_dt)) return st;
@@ -252,8 +261,9 @@ coded_status coded_sizes(const coded_code* c, coded_dtype dt, coded_dtype y_dt, 
     if (parity_bytes)
         *parity_bytes = static_cast<int64_t>(c->planes) * (c->n - c->k) * qb * r * static_cast<int64_t>(dtype_size(dt));
     if (y_bytes) *y_bytes = static_cast<int64_t>(c->n) * qb * s * static_cast<int64_t>(dtype_size(y_dt));
-    if (workspace_bytes)
-        *workspace_bytes = static_cast<int64_t>(c->n) * qb * s * (dt == CODED_F32 ? 8 : 4);
+    const int64_t wws = dt == CODED_BF16 ? worker_workspace_bytes_bf16(r, s) : 0;
+    if (workspace_bytes) *workspace_bytes = matmul_y_bytes(c, dt, q, s) + wws;
+    if (worker_workspace_bytes) *worker_workspace_bytes = wws;
     return CODED_OK;
     CODED_GUARD_END
 }
@@ -270,12 +280,13 @@ coded_status coded_encode(const coded_code* c, coded_dtype dt, const void* A, in
 
 coded_status coded_worker_mm(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                              const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* worker_mask,
-                             void* Y, coded_dtype y_dt, void* stream) {
+                             void* Y, coded_dtype y_dt, void* workspace, void* stream) {
     CODED_GUARD_BEGIN
     if (coded_status st = check_code(c)) return st;
     if (coded_status st = check_dt(dt, y_dt)) return st;
     if (coded_status st = check_ar(q, r, lda)) return st;
-    return do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, worker_mask, Y, y_dt, static_cast<hipStream_t>(stream));
+    return do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, worker_mask, Y, y_dt, workspace,
+                      static_cast<hipStream_t>(stream));
     CODED_GUARD_END
 }
 
@@ -387,7 +398,8 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
 
     if (!parity_ready)
         if (coded_status s2 = do_encode(c, dt, A, q, r, lda, parity, st)) return s2;
-    if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, workspace, y_dt, st)) return s2;
+    void* wws = static_cast<char*>(workspace) + matmul_y_bytes(c, dt, q, s);
+    if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, workspace, y_dt, wws, st)) return s2;
     if (coded_status s2 = do_decode_single(c, set, m, workspace, y_dt, q, s, out, ldo, info, st)) return s2;
     if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
     if (t_overall_out) *t_overall_out = t;
@@ -452,10 +464,10 @@ coded_status coded_gd_step(const coded_code* cA, const coded_code* cT, const flo
     float* z = reinterpret_cast<float*>(reinterpret_cast<char*>(Y2) +
                                         align256(static_cast<int64_t>(cT->n) * block_rows(r, cT->k) * 8));
     // z = A x - y  (coded product with code A, residual fused into the decode)
-    if (coded_status e = do_workers(cA, CODED_F32, A, q, r, lda, parityA, x, 1, 1, nullptr, Y1, CODED_F64, st)) return e;
+    if (coded_status e = do_workers(cA, CODED_F32, A, q, r, lda, parityA, x, 1, 1, nullptr, Y1, CODED_F64, nullptr, st)) return e;
     if (coded_status e = do_decode_single(cA, set1, m1, Y1, CODED_F64, q, 1, z, 1, info, st, y, 1.0, -1.0)) return e;
     // x = x - eta A^T z  (coded product with the code of A^T, update fused into the decode)
-    if (coded_status e = do_workers(cT, CODED_F32, AT, r, q, ldat, parityAT, z, 1, 1, nullptr, Y2, CODED_F64, st)) return e;
+    if (coded_status e = do_workers(cT, CODED_F32, AT, r, q, ldat, parityAT, z, 1, 1, nullptr, Y2, CODED_F64, nullptr, st)) return e;
     if (coded_status e = do_decode_single(cT, set2, m2, Y2, CODED_F64, r, 1, x, 1, info + 1, st, x, -eta, 1.0)) return e;
     if (survivors_out) {
         std::copy(s1, s1 + cA->k, survivors_out);

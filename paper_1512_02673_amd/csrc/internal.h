@@ -47,11 +47,14 @@ struct WorkerArgs {
     int32_t n, k, planes;
     int32_t y_f64;        // 1: Y is fp64, 0: Y is fp32
     int32_t n_sys, n_par; // active systematic / parity workers
+    void* xt;             // bf16 only: scratch for X transposed (s x r), or null
     uint8_t sys_ids[kMaxN];
     uint8_t par_ids[kMaxN];
 };
 hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st);
 hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
+// Bytes of the bf16 worker workspace (X transposed), 256-byte aligned.
+int64_t worker_workspace_bytes_bf16(int64_t r, int64_t s);
 
 // ---------------------------------------------------------------- decode
 // One survivor set passed by value (worker indices < 128 fit in a byte;

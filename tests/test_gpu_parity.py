@@ -149,6 +149,26 @@ def test_worker_products_gaussian(lib, torch, n, k, q, r, s, planes):
     assert np.all(err[k:] <= (1e-12 + parity_u) * bound[k:])
 
 
+@pytest.mark.parametrize("n,k,q,r,s", [(32, 24, 1000, 512, 64), (32, 24, 333, 136, 40), (6, 4, 70, 256, 16),
+                                       (5, 3, 31, 64, 7), (8, 5, 90, 128, 100), (4, 2, 10, 8, 1), (5, 3, 20, 12, 3)])
+@pytest.mark.parametrize("planes", [1, 2])
+def test_worker_products_bf16_integer_bit_exact(lib, torch, n, k, q, r, s, planes):
+    """bf16 blocks and X on the matrix cores (and the vector kernel without a workspace):
+    integer-valued inputs make every fp32 sum exact, so Y must equal the oracle's exactly."""
+    P, A, X = make_inputs(n, k, q, r, s, 19, "bf16", integer=True)
+    code = lib.Code.systematic(P, planes)
+    dA, dX = device_tensor(A, "bf16"), device_tensor(X[:, 0] if s == 1 else X, "bf16")
+    par = lib.alloc_parity(code, q, r, torch.bfloat16)
+    lib.coded_encode(code, dA, par)
+    ref = oc.worker_products(oc.encode(oc.systematic_generator(P), oc.pad_and_split(A, k)), X)
+    for ws in ("auto", None):
+        Y = lib.alloc_y(code, q, s, torch.float32)
+        Y.fill_(float("nan"))
+        lib.coded_worker_mm(code, dA, par, dX, Y, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(Y.cpu().numpy().astype(np.float64), ref), ws
+
+
 def test_worker_mask_leaves_other_rows_untouched(lib, torch):
     n, k, q, r = 16, 12, 500, 640
     P, A, X = make_inputs(n, k, q, r, 1, 8, integer=True)
@@ -306,8 +326,7 @@ def test_decode_batched_matches_single(lib, torch):
 
 def run_matmul(lib, torch, code, dA, par, dX, q, s, seed, draw, parity_ready):
     out = torch.empty((q, s) if s > 1 else (q,), dtype=torch.float32, device="cuda")
-    ws = torch.empty((code.n, code.qb(q), s), dtype=torch.float64 if dA.dtype == torch.float32 else torch.float32,
-                     device="cuda")
+    ws = lib.matmul_workspace(code, dA, dX)
     info = info_tensor(torch)
     surv, t = lib.coded_matmul(code, dA, par, dX, out, ws, info, seed, draw, parity_ready=parity_ready)
     torch.cuda.synchronize()

@@ -135,3 +135,34 @@ def test_gd_workload_full_size(lib, torch):
     xf = x.cpu().numpy().astype(np.float64)
     grad = A64.T @ (A64 @ xf - y64)
     assert np.linalg.norm(grad) <= 1e-4 * np.linalg.norm(A64.T @ y64)
+
+
+def test_dense_bf16_workload_full_size(lib, torch):
+    """(32,24) code, A 131072 x 16384 bf16, X 16384 x 64 bf16, fp32 accumulation: two full calls
+    (encode + matrix-core worker products + decode); sampled block rows of every block against
+    the oracle's fp64 product (max normwise error 2e-2), survivors against the oracle."""
+    w = synth.WORKLOADS["gemm_bf16_32x24_131072x16384x64"]
+    n, k, q, r, s, seed = w.n, w.k, w.q, w.r, w.s, w.seed
+    A = synth.bf16_round(synth.gaussian_rows(q, r, seed, synth.STREAM_A))
+    P = synth.parity_matrix(n, k, seed, dtype="bf16")
+    code = lib.Code.systematic(P, 2)
+    dA = torch.from_numpy(synth.bf16_bits(A).view(np.int16)).cuda().view(torch.bfloat16)
+    par = lib.alloc_parity(code, q, r, torch.bfloat16)
+    out = torch.empty((q, s), dtype=torch.float32, device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    qb = code.qb(q)
+    rng = np.random.default_rng(0)
+    for t in range(2):
+        X = synth.bf16_round(synth.gaussian((r, s), seed, synth.STREAM_X, t))
+        dX = torch.from_numpy(synth.bf16_bits(X).view(np.int16)).cuda().view(torch.bfloat16)
+        ws = lib.matmul_workspace(code, dA, dX)
+        surv, _ = lib.coded_matmul(code, dA, par, dX, out, ws, info, seed, t, parity_ready=False)
+        torch.cuda.synchronize()
+        assert np.array_equal(surv, oc.draw_survivors(n, k, seed, t)[0]) and int(info.item()) == 0
+        ts = rng.choice(qb, size=24, replace=False)
+        rows = np.array([j * qb + tt for j in range(k) for tt in ts if j * qb + tt < q])
+        ref = oc.plain_product(A[rows], X)
+        got = out.cpu().numpy()[rows].astype(np.float64)
+        full_ref_scale = np.max(np.abs(ref), axis=0)
+        err = float(np.max(np.max(np.abs(got - ref), axis=0) / full_ref_scale))
+        assert err <= 2e-2, err
