@@ -105,20 +105,22 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
     __shared__ double red[NW][T];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t groups = ceil_div(a.qb, T);
-    const int64_t nsys = groups * a.n_sys;
+    const int64_t npar = groups * a.n_par;
     const int64_t g = blockIdx.x;
     int worker;
     int64_t grp;
     bool parity;
-    if (g < nsys) {
-        worker = a.sys_ids[g / groups];
+    // Parity workgroups stream `planes` times the bytes: dispatch them first so
+    // the launch does not end on a tail of long workgroups.
+    if (g < npar) {
+        worker = a.par_ids[g / groups];
         grp = g % groups;
-        parity = false;
-    } else {
-        if (g - nsys >= groups * a.n_par) return;
-        worker = a.par_ids[(g - nsys) / groups];
-        grp = (g - nsys) % groups;
         parity = true;
+    } else {
+        if (g - npar >= groups * a.n_sys) return;
+        worker = a.sys_ids[(g - npar) / groups];
+        grp = (g - npar) % groups;
+        parity = false;
     }
     const int64_t t0 = grp * T;
     const int nplanes = parity ? a.planes : 1;
@@ -284,25 +286,27 @@ __global__ __launch_bounds__(kThreads) void gemm_small_bf16_kernel(WorkerArgs a)
 // lane l element e = B[8*(l/16)+e][l%16], result lane l item v =
 // C[4*(l/16)+v][l%16].  Both operands are read along K in 16-byte pieces, so
 // X is first transposed (X^T, s x r) into the workspace.  A workgroup of four
-// wavefronts owns 4*SLABS*16 rows of one worker's block; each K chunk of X^T
-// (64 columns x kBK) is staged in LDS once and shared by all of them.  A
-// parity row's hi and lo planes accumulate into the same tile.  Parity
+// wavefronts owns 4*SLABS*16 rows of one worker's block.  X^T is staged in
+// LDS in K chunks of kBK, double-buffered: the next chunk is read into
+// registers while the current one feeds the matrix cores, so each chunk costs
+// one barrier.  A fragments are plain 16-byte loads: each instruction reads
+// 64 bytes of 16 rows, and the other half of every 128-byte line is read by
+// the next instruction, which a non-temporal hint would evict first.  A
+// parity row's hi and lo planes accumulate into the same tile; parity
 // workgroups (twice the bytes) are scheduled first.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kBK = 128;     // K chunk staged in LDS
-constexpr int kXPad = 8;     // bf16 padding per LDS row (keeps the 16-byte reads spread over banks)
-
-__device__ inline bf16x8 load_bf16x8_stream(const uint16_t* p) {
-    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
-}
+constexpr int kBK = 64;      // K chunk of X^T staged in LDS
+constexpr int kXPad = 8;     // bf16 padding per LDS row (spreads the 16-byte reads over banks)
 
 template <int NTILE, int SLABS>
 __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, int64_t tiles, int64_t c0) {
     constexpr int ROWS = kWaves * SLABS * 16;
-    __shared__ __align__(16) uint16_t sXT[16 * NTILE][kBK + kXPad];
+    constexpr int KS = kBK / 32;
+    constexpr int XV = (16 * NTILE * (kBK / 8) + kThreads - 1) / kThreads;   // X^T vectors per thread per chunk
+    __shared__ __align__(16) uint16_t sXT[2][16 * NTILE][kBK + kXPad];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int li = lane & 15, lk = lane >> 4;
     const int64_t g = blockIdx.x;
@@ -322,6 +326,7 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
     const int nplanes = parity ? a.planes : 1;
     const int64_t plane = static_cast<int64_t>(a.n - a.k) * a.qb * a.r;
     const uint16_t* XT = static_cast<const uint16_t*>(a.xt);
+    const int64_t ncols = min<int64_t>(16 * NTILE, a.s - c0);
     const uint16_t* rp[SLABS][2];
     int64_t trow[SLABS];
 #pragma unroll
@@ -347,33 +352,51 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
 #pragma unroll
         for (int j = 0; j < NTILE; ++j) acc[sl][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const bf16x8 zero8 = __builtin_bit_cast(bf16x8, u32x4_t{0u, 0u, 0u, 0u});
-    const int64_t ncols = min<int64_t>(16 * NTILE, a.s - c0);
 
-    for (int64_t kc = 0; kc < a.r; kc += kBK) {
-        bf16x8 af[kBK / 32][SLABS][2];
+    u32x4_t xr[XV];
+    auto xload = [&](int64_t kc) {
 #pragma unroll
-        for (int ks = 0; ks < kBK / 32; ++ks) {
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + kThreads * i;
+            const int col = e / (kBK / 8), v = e % (kBK / 8);
+            const int64_t k = kc + 8 * v;
+            xr[i] = (col < ncols && k < a.r) ? *reinterpret_cast<const u32x4_t*>(XT + (c0 + col) * a.r + k)
+                                             : u32x4_t{0u, 0u, 0u, 0u};
+        }
+    };
+    auto xstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + kThreads * i;
+            const int col = e / (kBK / 8), v = e % (kBK / 8);
+            if (col < 16 * NTILE) *reinterpret_cast<u32x4_t*>(&sXT[buf][col][8 * v]) = xr[i];
+        }
+    };
+    xload(0);
+    xstore(0);
+    __syncthreads();
+    int buf = 0;
+    for (int64_t kc = 0; kc < a.r; kc += kBK) {
+        bf16x8 af[KS][SLABS][2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
             const int64_t k = kc + 32 * ks + 8 * lk;
 #pragma unroll
             for (int sl = 0; sl < SLABS; ++sl)
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
-                    af[ks][sl][h] = (rp[sl][h] && h < nplanes && k < a.r) ? load_bf16x8_stream(rp[sl][h] + k) : zero8;
+                    af[ks][sl][h] = (rp[sl][h] && h < nplanes && k < a.r)
+                                        ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4_t*>(rp[sl][h] + k))
+                                        : zero8;
         }
-        __syncthreads();
-        for (int e = tid; e < 16 * NTILE * (kBK / 8); e += kThreads) {
-            const int col = e / (kBK / 8), v = e % (kBK / 8);
-            const int64_t k = kc + 8 * v;
-            u32x4_t val = u32x4_t{0u, 0u, 0u, 0u};
-            if (col < ncols && k < a.r) val = *reinterpret_cast<const u32x4_t*>(XT + (c0 + col) * a.r + k);
-            *reinterpret_cast<u32x4_t*>(&sXT[col][8 * v]) = val;
-        }
-        __syncthreads();
+        const bool more = kc + kBK < a.r;
+        if (more) xload(kc + kBK);
 #pragma unroll
-        for (int ks = 0; ks < kBK / 32; ++ks) {
+        for (int ks = 0; ks < KS; ++ks) {
             bf16x8 bfr[NTILE];
 #pragma unroll
-            for (int j = 0; j < NTILE; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(&sXT[16 * j + li][32 * ks + 8 * lk]);
+            for (int j = 0; j < NTILE; ++j)
+                bfr[j] = *reinterpret_cast<const bf16x8*>(&sXT[buf][16 * j + li][32 * ks + 8 * lk]);
 #pragma unroll
             for (int sl = 0; sl < SLABS; ++sl)
 #pragma unroll
@@ -383,6 +406,9 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
                         for (int j = 0; j < NTILE; ++j)
                             acc[sl][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ks][sl][h], bfr[j], acc[sl][j], 0, 0, 0);
         }
+        if (more) xstore(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
     }
     float* Y = static_cast<float*>(a.Y);
 #pragma unroll
