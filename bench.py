@@ -32,7 +32,8 @@ import synth  # noqa: E402
 METRIC = "coded A·X decoded products/sec + achieved HBM GB/s (GEMV) / MFMA % (GEMM)"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "worker_gemv_traffic_gemv16x12.json")
-KERNEL_SOURCES = ["paper_1512_02673_amd/csrc/worker.hip", "paper_1512_02673_amd/csrc/internal.h"]
+KERNEL_SOURCES = ["paper_1512_02673_amd/csrc/worker.hip", "paper_1512_02673_amd/csrc/worker_common.h",
+                  "paper_1512_02673_amd/csrc/internal.h"]
 
 
 def kernel_source_hash() -> str:
