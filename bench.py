@@ -510,6 +510,58 @@ def cpu_baseline_dense(w, A, Xs, P, t, out_dev, qb, rows):
             "gpu_vs_oracle_max_rel_err_on_sample": err}
 
 
+def runtime_sim_workload(args):
+    """Runtime model of Sec. III-C/III-D at the setting of its runtime-distribution
+    figure (n = 10, k = 5, shift 1, rate 1): one step simulates 16M draws and
+    writes the uncoded, 2-repetition and (10,5) MDS overall runtimes of each."""
+    import torch
+
+    from paper_1512_02673_amd import binding as lib
+
+    n, k, seed, draws = 10, 5, 6, 1 << 24
+    K, W = args.steps, args.warmup
+    out = [torch.empty(draws, dtype=torch.float64, device="cuda") for _ in range(3)]
+    stream = torch.cuda.current_stream()
+    for t in range(W):
+        lib.coded_simulate_runtimes(n, k, seed, t * draws, *out)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    start = time.perf_counter()
+    for i in range(K):
+        evs[i][0].record(stream)
+        lib.coded_simulate_runtimes(n, k, seed, (W + i) * draws, *out)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - start
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    means = [float(t.mean().item()) for t in out]
+    wbytes = 24.0 * draws
+    result = {
+        "metric": METRIC, "value": K * draws / elapsed, "unit": "simulated draws/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "runtime_sim_10x5", "n": n, "k": k, "shift": 1.0, "rate": 1.0,
+                   "draws_per_step": draws, "schemes": ["uncoded", "repetition", "mds"]},
+        "means_last_step": dict(zip(["uncoded", "repetition", "mds"], means)),
+        "roofline": {"bound": "alu", "kernel": "runtime_sim_kernel",
+                     "note": "integer-ALU bound: 64-bit SplitMix64 words and O(n^2) ranking per draw; "
+                             "the output writes use only the fraction of HBM given here",
+                     "achieved": wbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": wbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "algorithmic_bytes_per_launch": wbytes, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import runtime as rt
+        cnt = 1 << 21
+        t0 = time.perf_counter()
+        rt.simulate(n, k, seed, 0, cnt)
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": cnt / el, "unit": "simulated draws/s", "cores": blas_threads(),
+                                  "kind": "oracle", "sample": f"{cnt} draws of the same simulation with the NumPy "
+                                                              f"oracle in {el:.1f} s"}
+    return result
+
+
 def calibrate_copy(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -528,7 +580,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
                     choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8", "gd20x16_262144x4096",
-                             "gemm_bf16_32x24_131072x16384x64"])
+                             "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-products", type=int, default=300)
     ap.add_argument("--cpu-decodes", type=int, default=1000)
@@ -560,6 +612,12 @@ def main():
         if "--warmup" not in sys.argv:
             args.warmup = 3
         result = dense_bf16_workload(args)
+    elif args.workload == "runtime_sim_10x5":
+        if "--steps" not in sys.argv:
+            args.steps = 20
+        if "--warmup" not in sys.argv:
+            args.warmup = 2
+        result = runtime_sim_workload(args)
     elif args.workload == "gd20x16_262144x4096":
         if "--steps" not in sys.argv:
             args.steps = 200

@@ -257,6 +257,34 @@ coded_status coded_gd_step(const coded_code* codeA, const coded_code* codeAT, co
                            double shift, double rate, void* workspace, int32_t* info, int32_t* survivors_out,
                            void* stream);
 
+/*
+ * coded_simulate_runtimes -- Monte-Carlo of the runtime model of Sec. III-B
+ * to III-D.  Draw d (first_draw <= d < first_draw + count) gives worker i the
+ * mother-runtime sample T0 = shift - ln(U)/rate from the same SplitMix64 word
+ * as coded_draw_survivors, and the overall runtime of one job under:
+ *   t_uncoded[d]     n subtasks of T0/n: the slowest (eq. uncoded);
+ *   t_repetition[d]  k tasks of T0/k, each replicated on n/k consecutive
+ *                    workers: the slowest task's fastest replica (eq.
+ *                    rep_coded); requires k | n;
+ *   t_mds[d]         (n,k) MDS, tasks of T0/k: the k-th finisher (eq.
+ *                    mds_coded; equals coded_draw_survivors' T_(k)).
+ * Output pointers are device fp64[count]; any may be NULL to skip a scheme.
+ */
+coded_status coded_simulate_runtimes(int32_t n, int32_t k, uint64_t seed, uint64_t first_draw, int64_t count,
+                                     double shift, double rate, double* t_uncoded, double* t_repetition,
+                                     double* t_mds, void* stream);
+
+/*
+ * coded_optimal_k -- host only.  Lemma 2 (Sec. III-D): with the shifted-
+ * exponential model (shift 1, straggling parameter rate), the expected MDS
+ * runtime is minimised by k* = [1 + 1/W_{-1}(-e^{-rate-1})] n, with value
+ * T* = -W_{-1}(-e^{-rate-1}) / (rate n), where W_{-1} is the lower branch of
+ * Lambert W.  k_best is the integer k in [1, n] minimising the exact expected
+ * runtime (1/k)(1 + (H_n - H_{n-k})/rate) (smallest k on ties).  Any output
+ * pointer may be NULL.
+ */
+coded_status coded_optimal_k(int32_t n, double rate, double* k_star, double* t_star, int32_t* k_best);
+
 /* Static text of a status code. */
 const char* coded_status_string(coded_status status);
 /* Message of the last failing call on this thread ("" if none). */

@@ -43,6 +43,9 @@ _SIGNATURES = {
     "coded_gd_sizes": (_c_i32, [_c_p, _c_p, _c_i64, _c_i64, _c_p]),
     "coded_gd_step": (_c_i32, [_c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_dbl,
                                _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_p]),
+    "coded_simulate_runtimes": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_i64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p,
+                                         _c_p]),
+    "coded_optimal_k": (_c_i32, [_c_i32, _c_dbl, _c_p, _c_p, _c_p]),
     "coded_status_string": (ctypes.c_char_p, [_c_i32]),
     "coded_last_error": (ctypes.c_char_p, []),
     "coded_version": (ctypes.c_char_p, []),
@@ -114,6 +117,13 @@ def coded_draw_survivor_sets(n: int, k: int, seed: int, batch: int, min_parity: 
     _check(lib().coded_draw_survivor_sets(n, k, seed, first_draw, batch, min_parity, out.ctypes.data,
                                           ctypes.addressof(nxt)))
     return out, nxt.value
+
+
+def coded_optimal_k(n: int, rate: float):
+    """(k*, T*, best integer k) of Lemma 2."""
+    ks, ts, kb = ctypes.c_double(), ctypes.c_double(), ctypes.c_int32()
+    _check(lib().coded_optimal_k(n, rate, ctypes.addressof(ks), ctypes.addressof(ts), ctypes.addressof(kb)))
+    return ks.value, ts.value, kb.value
 
 
 # ---------------------------------------------------------------- device calls
@@ -293,6 +303,19 @@ def coded_gd_step(codeA: Code, codeAT: Code, A, parityA, AT, parityAT, y, x, eta
                                _ptr(parityAT), q, r, _ptr(y), _ptr(x), eta, seed, iteration, shift, rate,
                                _ptr(workspace), _ptr(info), surv.ctypes.data_as(ctypes.c_void_p), _stream(stream)))
     return surv[:codeA.k], surv[codeA.k:]
+
+
+def coded_simulate_runtimes(n: int, k: int, seed: int, first_draw: int, t_uncoded=None, t_repetition=None,
+                            t_mds=None, shift: float = 1.0, rate: float = 1.0, stream=None) -> None:
+    """Fill the given device fp64 tensors (equal lengths) with per-draw overall runtimes."""
+    outs = [t for t in (t_uncoded, t_repetition, t_mds) if t is not None]
+    if not outs:
+        return
+    count = outs[0].numel()
+    if any(t.numel() != count for t in outs):
+        raise ValueError("output tensors must have equal lengths")
+    _check(lib().coded_simulate_runtimes(n, k, seed, first_draw, count, shift, rate, _ptr(t_uncoded),
+                                         _ptr(t_repetition), _ptr(t_mds), _stream(stream)))
 
 
 # ---------------------------------------------------------------- buffer helpers

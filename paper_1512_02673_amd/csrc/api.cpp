@@ -477,6 +477,45 @@ coded_status coded_gd_step(const coded_code* cA, const coded_code* cT, const flo
     CODED_GUARD_END
 }
 
+coded_status coded_simulate_runtimes(int32_t n, int32_t k, uint64_t seed, uint64_t first_draw, int64_t count,
+                                     double shift, double rate, double* t_uncoded, double* t_repetition, double* t_mds,
+                                     void* stream) {
+    CODED_GUARD_BEGIN
+    if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
+    if (count < 0) return fail(CODED_ERR_ARG, "count must be >= 0");
+    if (!(rate > 0.0) || !std::isfinite(shift)) return fail(CODED_ERR_ARG, "need rate > 0 and a finite shift");
+    if (first_draw + static_cast<uint64_t>(count) > (1ull << 40)) return fail(CODED_ERR_ARG, "draws must stay below 2^40");
+    if (t_repetition && n % k != 0) return fail(CODED_ERR_ARG, "repetition needs k to divide n");
+    hipError_t e = launch_runtime_sim(n, k, seed, first_draw, count, shift, rate, t_uncoded, t_repetition, t_mds,
+                                      static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "runtime simulation launch");
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_optimal_k(int32_t n, double rate, double* k_star, double* t_star, int32_t* k_best) {
+    CODED_GUARD_BEGIN
+    if (n < 1) return fail(CODED_ERR_ARG, "n must be >= 1");
+    if (!(rate > 0.0) || !std::isfinite(rate)) return fail(CODED_ERR_ARG, "rate must be > 0");
+    const double w = coded_rng::lambert_w_lower(-std::exp(-rate - 1.0));
+    if (k_star) *k_star = (1.0 + 1.0 / w) * n;
+    if (t_star) *t_star = -w / (rate * n);
+    if (k_best) {
+        // exact expected MDS runtime (1/k)(1 + (H_n - H_{n-k})/rate), smallest over integer k
+        std::vector<double> H(n + 1, 0.0);
+        for (int i = 1; i <= n; ++i) H[i] = H[i - 1] + 1.0 / i;
+        int best = 1;
+        double bv = 1e300;
+        for (int kk = 1; kk <= n; ++kk) {
+            const double v = (1.0 + (H[n] - H[n - kk]) / rate) / kk;
+            if (v < bv) { bv = v; best = kk; }
+        }
+        *k_best = best;
+    }
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
 const char* coded_status_string(coded_status status) {
     switch (status) {
         case CODED_OK: return "CODED_OK";

@@ -84,6 +84,10 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax,
 hipError_t launch_transpose_f32(const float* A, int64_t q, int64_t r, int64_t lda, float* AT, int64_t ldat,
                                 hipStream_t st);
 
+// ---------------------------------------------------------------- runtime model
+hipError_t launch_runtime_sim(int n, int k, uint64_t seed, uint64_t first, int64_t count, double shift, double rate,
+                              double* t_uncoded, double* t_repetition, double* t_mds, hipStream_t st);
+
 }  // namespace coded
 
 // Host runtime model (survivors.cpp); plain C++, no device code.
@@ -92,4 +96,6 @@ uint64_t splitmix64_output(uint64_t seed, uint64_t index);
 uint64_t runtime_word(uint64_t seed, uint64_t stream, uint64_t draw, uint64_t worker);
 // Survivors of one draw: k worker indices ascending; returns T_(k).
 double draw_survivors(int n, int k, uint64_t seed, uint64_t draw, double shift, double rate, int32_t* out);
+// W_{-1}(x) for -1/e <= x < 0 (lower real branch of Lambert W).
+double lambert_w_lower(double x);
 }  // namespace coded_rng

@@ -51,4 +51,27 @@ double draw_survivors(int n, int k, uint64_t seed, uint64_t draw, double shift, 
     return (shift + (-std::log(u)) / rate) / static_cast<double>(k);
 }
 
+double lambert_w_lower(double x) {
+    // Halley's iteration on f(w) = w e^w - x, started from the branch-point
+    // series near -1/e or from the asymptotic logarithmic form near 0.
+    const double e = 2.718281828459045235;
+    if (x <= -1.0 / e) return -1.0;
+    double w;
+    if (x < -0.25) {
+        const double p = -std::sqrt(2.0 * (1.0 + e * x));
+        w = -1.0 + p - p * p / 3.0;
+    } else {
+        const double lx = std::log(-x);
+        w = lx - std::log(-lx);
+    }
+    for (int it = 0; it < 100; ++it) {
+        const double ew = std::exp(w), f = w * ew - x, wp1 = w + 1.0;
+        if (wp1 == 0.0) break;
+        const double step = f / (ew * wp1 - (w + 2.0) * f / (2.0 * wp1));
+        w -= step;
+        if (std::fabs(step) <= 1e-15 * std::fabs(w)) break;
+    }
+    return w;
+}
+
 }  // namespace coded_rng

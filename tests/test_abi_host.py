@@ -74,3 +74,12 @@ def test_host_argument_errors(lib):
         lib.CODED_ERR_ARG
     assert h.coded_encode(None, 0, None, 0, 0, 1, None, None) == lib.CODED_ERR_ARG
     assert h.coded_decode(None, None, 0, None, 2, 0, 0, None, 1, None, None) == lib.CODED_ERR_ARG
+
+
+@pytest.mark.parametrize("n,mu", [(10, 1.0), (100, 0.5), (1000, 1.0), (64, 2.0), (7, 0.1)])
+def test_optimal_k_matches_oracle(lib, n, mu):
+    from oracle import runtime as rt
+    ks, ts, kb = lib.coded_optimal_k(n, mu)
+    ks_ref, ts_ref, _ = rt.optimal_mds(n, mu)
+    assert ks == pytest.approx(ks_ref, rel=1e-12) and ts == pytest.approx(ts_ref, rel=1e-12)
+    assert kb == rt.best_integer_k(n, mu)
