@@ -289,7 +289,7 @@ def decode_workload(args):
         "dtype": "f64", "data": "synthetic",
         "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "s": s, "sets_per_step": B,
                    "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean())},
-        "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
                      "traffic": None, "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12},
     }

@@ -33,6 +33,8 @@ namespace {
 
 constexpr int kThreads = 256;
 
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
 __device__ inline int set_entry(const DecodeSet& s, int c) {
     // Pick byte c of the packed set with constant-index reads of the argument.
     uint32_t word = 0;
@@ -68,11 +70,9 @@ struct Vec<4, float> {
 
 // out = v, or alpha * v + beta * c when an epilogue operand is given (c has
 // out's layout; the element is read before it is written, so c may be out).
-template <int E>
-__device__ inline void store_out(const DecodeArgs& a, float* p, int64_t off, const double* v) {
-    double w[E];
-#pragma unroll
-    for (int i = 0; i < E; ++i) w[i] = v[i];
+template <int E, typename T>
+__device__ inline void store_out(const DecodeArgs& a, float* p, int64_t off, const T* v) {
+    float w[E];
     if (a.c) {
         float cv[E];
         if constexpr (E == 4) {
@@ -82,13 +82,96 @@ __device__ inline void store_out(const DecodeArgs& a, float* p, int64_t off, con
             cv[0] = a.c[off];
         }
 #pragma unroll
-        for (int i = 0; i < E; ++i) w[i] = fma(a.alpha, w[i], a.beta * static_cast<double>(cv[i]));
+        for (int i = 0; i < E; ++i)
+            w[i] = static_cast<float>(fma(a.alpha, static_cast<double>(v[i]), a.beta * static_cast<double>(cv[i])));
+    } else {
+#pragma unroll
+        for (int i = 0; i < E; ++i) w[i] = static_cast<float>(v[i]);
     }
-    if constexpr (E == 4)
-        *reinterpret_cast<float4*>(p + off) = make_float4(static_cast<float>(w[0]), static_cast<float>(w[1]),
-                                                          static_cast<float>(w[2]), static_cast<float>(w[3]));
-    else
-        p[off] = static_cast<float>(w[0]);
+    // decoded outputs are written once and not read again here: non-temporal
+    if constexpr (E == 4) {
+        const f32x4v q = {w[0], w[1], w[2], w[3]};
+        __builtin_nontemporal_store(q, reinterpret_cast<f32x4v*>(p + off));
+    } else {
+        __builtin_nontemporal_store(w[0], p + off);
+    }
+}
+
+// E consecutive elements of Y as fp32 (a copied systematic block is the
+// worker's result rounded to the output type).
+template <int E, typename YT>
+__device__ inline void load_f32(const YT* p, float* v) {
+    if constexpr (E == 4 && sizeof(YT) == 4) {
+        const float4 f = *reinterpret_cast<const float4*>(p);
+        v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    } else if constexpr (E == 4) {
+        const double2 lo = reinterpret_cast<const double2*>(p)[0], hi = reinterpret_cast<const double2*>(p)[1];
+        v[0] = static_cast<float>(lo.x); v[1] = static_cast<float>(lo.y);
+        v[2] = static_cast<float>(hi.x); v[3] = static_cast<float>(hi.y);
+    } else {
+        v[0] = static_cast<float>(p[0]);
+    }
+}
+
+// Per-set bookkeeping in LDS, shared by both decode kernels.
+struct SetMeta {
+    int32_t raw[kMaxN];
+    int32_t S[kMaxN];          // sorted survivors
+    int32_t present[kMaxN];
+    int32_t miss[kMaxN];       // missing systematic blocks, ascending
+    int64_t yoff[kMaxN];       // element offset of survivor c's result in Y
+    int64_t ooff[kMaxN];       // element offset of block j's first row in out
+    int32_t lim[kMaxN];        // rows of block j that lie inside A (the rest is padding)
+    int32_t status, m;
+};
+
+// Reads set b, validates it (range, repeats), sorts it and fills the
+// bookkeeping.  Returns false (after writing info = -1) for an invalid set.
+// Every thread of the workgroup must call it.
+__device__ __forceinline__ bool setup_set(const DecodeArgs& a, const DecodeSet& single, int64_t b, bool writer, SetMeta& sm) {
+    const int tid = threadIdx.x;
+    const int n = a.n, k = a.k;
+    if (tid == 0) sm.status = 0;
+    for (int i = tid; i < n; i += kThreads) sm.present[i] = 0;
+    for (int c = tid; c < k; c += kThreads) sm.raw[c] = a.sets ? a.sets[b * k + c] : set_entry(single, c);
+    __syncthreads();
+    for (int c = tid; c < k; c += kThreads) {
+        const int v = sm.raw[c];
+        if (v < 0 || v >= n) {
+            sm.status = -1;
+            continue;
+        }
+        int rank = 0, same = 0;
+        for (int j = 0; j < k; ++j) {
+            rank += sm.raw[j] < v;
+            same += sm.raw[j] == v;
+        }
+        if (same != 1) {
+            sm.status = -1;
+            continue;
+        }
+        sm.S[rank] = v;
+        sm.present[v] = 1;
+    }
+    __syncthreads();
+    if (sm.status != 0) {
+        if (writer) a.info[b] = sm.status;
+        return false;
+    }
+    if (tid == 0) {
+        int m = 0;
+        for (int j = 0; j < k; ++j)
+            if (!sm.present[j]) sm.miss[m++] = j;
+        sm.m = m;
+    }
+    for (int c = tid; c < k; c += kThreads) sm.yoff[c] = static_cast<int64_t>(sm.S[c]) * a.qb * a.s;
+    for (int j = tid; j < k; j += kThreads) {
+        sm.ooff[j] = static_cast<int64_t>(j) * a.qb * a.ldo;
+        const int64_t lim = a.q - static_cast<int64_t>(j) * a.qb;
+        sm.lim[j] = static_cast<int32_t>(lim < 0 ? 0 : (lim > a.qb ? a.qb : lim));
+    }
+    __syncthreads();
+    return true;
 }
 
 // PASS: missing outputs computed per sweep over the survivors (register
@@ -97,68 +180,24 @@ __device__ inline void store_out(const DecodeArgs& a, float* p, int64_t off, con
 template <int PASS, int E, typename YT>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
                                                           int elems_per_block, int ST) {
-    __shared__ int32_t sRaw[kMaxN];
-    __shared__ int32_t sS[kMaxN];        // sorted survivors
-    __shared__ int32_t sPresent[kMaxN];
-    __shared__ int32_t sMiss[kMaxN];     // missing systematic blocks, ascending
-    __shared__ int64_t sYoff[kMaxN];     // element offset of survivor c's result in Y
-    __shared__ int64_t sOoff[kMaxN];     // element offset of block j's first row in out
-    __shared__ int32_t sLim[kMaxN];      // rows of block j that lie inside A (the rest is padding)
-    __shared__ int32_t sStatus, sM;
+    __shared__ SetMeta sm;
     extern __shared__ __align__(16) double dyn[];
     double* sD = dyn;                    // D column-major: sD[c * ST + b], c < k
     double* sMat = dyn + a.k * ST;       // m x m, row stride ST
     double* sL = sMat + ST * ST;         // multipliers of one elimination step
 
     const int tid = threadIdx.x;
-    const int n = a.n, k = a.k;
+    const int k = a.k;
     const int64_t b = blockIdx.x / chunks;
     const int64_t chunk = blockIdx.x % chunks;
     const bool writer = (chunk == 0 && tid == 0);
-
-    if (tid == 0) sStatus = 0;
-    for (int i = tid; i < n; i += kThreads) sPresent[i] = 0;
-    for (int c = tid; c < k; c += kThreads) sRaw[c] = a.sets ? a.sets[b * k + c] : set_entry(single, c);
-    __syncthreads();
-
-    // Validate (range, repeats), sort by rank, mark present workers.
-    for (int c = tid; c < k; c += kThreads) {
-        const int v = sRaw[c];
-        if (v < 0 || v >= n) {
-            sStatus = -1;
-            continue;
-        }
-        int rank = 0, same = 0;
-        for (int j = 0; j < k; ++j) {
-            rank += sRaw[j] < v;
-            same += sRaw[j] == v;
-        }
-        if (same != 1) {
-            sStatus = -1;
-            continue;
-        }
-        sS[rank] = v;
-        sPresent[v] = 1;
-    }
-    __syncthreads();
-    if (sStatus != 0) {
-        if (writer) a.info[b] = sStatus;
-        return;
-    }
-    if (tid == 0) {
-        int m = 0;
-        for (int j = 0; j < k; ++j)
-            if (!sPresent[j]) sMiss[m++] = j;
-        sM = m;
-    }
-    for (int c = tid; c < k; c += kThreads) sYoff[c] = static_cast<int64_t>(sS[c]) * a.qb * a.s;
-    for (int j = tid; j < k; j += kThreads) {
-        sOoff[j] = static_cast<int64_t>(j) * a.qb * a.ldo;
-        const int64_t lim = a.q - static_cast<int64_t>(j) * a.qb;
-        sLim[j] = static_cast<int32_t>(lim < 0 ? 0 : (lim > a.qb ? a.qb : lim));
-    }
-    __syncthreads();
-    const int m = sM;
+    if (!setup_set(a, single, b, writer, sm)) return;
+    const int32_t* sS = sm.S;
+    const int32_t* sMiss = sm.miss;
+    const int64_t* sYoff = sm.yoff;
+    const int64_t* sOoff = sm.ooff;
+    const int32_t* sLim = sm.lim;
+    const int m = sm.m;
     const int first_par = k - m;          // sorted: systematic survivors first, then parity
 
     if (m > 0) {
@@ -193,12 +232,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
                         p = i;
                     }
                 }
-                if (best == 0.0) sStatus = first_par + j + 1;
-                sRaw[0] = p;                       // reuse: pivot row of this step
+                if (best == 0.0) sm.status = first_par + j + 1;
+                sm.raw[0] = p;                     // reuse: pivot row of this step
             }
             __syncthreads();
-            if (sStatus != 0) break;
-            const int p = sRaw[0];
+            if (sm.status != 0) break;
+            const int p = sm.raw[0];
             if (p != j) {
                 for (int c = tid; c < m; c += kThreads) {
                     const double t0 = sMat[j * ST + c];
@@ -220,26 +259,32 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
                     const int i = j + 1 + e / rows, c = j + 1 + e % rows;
                     sMat[i * ST + c] -= sL[i] * sMat[j * ST + c];
                 }
+                // consecutive threads walk down a column of D (contiguous in LDS)
                 for (int e = tid; e < rows * k; e += kThreads) {
-                    const int i = j + 1 + e / k, c = e % k;
+                    const int c = e / rows, i = j + 1 + e % rows;
                     sD[c * ST + i] -= sL[i] * sD[c * ST + j];
                 }
             }
             __syncthreads();
         }
-        if (sStatus != 0) {
-            if (writer) a.info[b] = sStatus;
+        if (sm.status != 0) {
+            if (writer) a.info[b] = sm.status;
             return;
         }
-        // Back substitution with U, one right-hand side column per thread.
-        for (int c = tid; c < k; c += kThreads) {
-            for (int i = m - 1; i >= 0; --i) {
-                double v = sD[c * ST + i];
-                for (int jj = i + 1; jj < m; ++jj) v -= sMat[i * ST + jj] * sD[c * ST + jj];
-                sD[c * ST + i] = v / sMat[i * ST + i];
+        // Back substitution with U, one step per pivot from the bottom: scale
+        // row i of D, then eliminate it from the rows above (consecutive
+        // threads walk down a column, contiguous in LDS).
+        for (int i = m - 1; i >= 0; --i) {
+            for (int c = tid; c < k; c += kThreads) sD[c * ST + i] /= sMat[i * ST + i];
+            __syncthreads();
+            if (i > 0) {
+                for (int e = tid; e < i * k; e += kThreads) {
+                    const int c = e / i, ii = e % i;
+                    sD[c * ST + ii] -= sMat[ii * ST + i] * sD[c * ST + i];
+                }
+                __syncthreads();
             }
         }
-        __syncthreads();
     }
     if (writer) a.info[b] = 0;
 
@@ -289,6 +334,241 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
     }
 }
 
+// ---------------------------------------------------------------- fast path
+// Codes with at most kFastM missing blocks per set and m + k <= 64: one wave
+// eliminates the m x (m + k) system [G[S_par, M] | -G[S_par, S_sys] | I] in
+// registers (Gauss-Jordan, partial pivoting: the same pivots as the LU above,
+// one column per lane, no workgroup barriers), and the combination of the
+// survivors is one 16-row matrix-core tile:
+//     out[M] (16 x 16 elements) += D (16 x 4 survivors) * Y (4 x 16 elements)
+// on v_mfma_f64_16x16x4f64, with D held in registers for the whole set.
+constexpr int kFastM = 16;
+constexpr int kFastLd = kFastM + 1;      // odd LDS column stride of D: spreads the banks
+typedef double f64x4v __attribute__((ext_vector_type(4)));
+
+__device__ inline double lane_value(double v, int lane) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(u), lane);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(u >> 32), lane);
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// Wave-level elimination.  Lane l holds column l of the augmented matrix:
+// lanes < m the columns of G[S_par, M], lanes m..m+k-1 the right-hand sides
+// (sorted survivor order).  On success D[b][c] = sD[c * kFastLd + b] (rows
+// >= m zero); on a zero pivot sm.status = first_par + j + 1.
+__device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm, int m, int first_par, int lane, double* sD) {
+    const int k = a.k;
+    const int c = lane - m;
+    double col[kFastM];
+#pragma unroll
+    for (int r = 0; r < kFastM; ++r) {
+        double v = 0.0;
+        if (r < m) {
+            const int64_t prow = static_cast<int64_t>(sm.S[first_par + r]) * k;
+            if (lane < m) {
+                v = a.G[prow + sm.miss[lane]];
+            } else if (c < k) {
+                const int sc = sm.S[c];
+                v = sc < k ? -a.G[prow + sc] : ((c - first_par == r) ? 1.0 : 0.0);
+            }
+        }
+        col[r] = v;
+    }
+    int status = 0;
+#pragma unroll
+    for (int j = 0; j < kFastM; ++j) {
+        // uniform guards instead of an early exit keep the loop fully unrolled
+        // (every register index a constant)
+        if (j < m && status == 0) {
+            // pivot: largest |entry| of column j in rows j..m-1, lowest row on ties
+            int p = j;
+            double best = fabs(col[j]);
+#pragma unroll
+            for (int i = j + 1; i < kFastM; ++i) {
+                const double v = fabs(col[i]);
+                if (i < m && v > best) {
+                    best = v;
+                    p = i;
+                }
+            }
+            p = __builtin_amdgcn_readlane(p, j);
+            best = lane_value(best, j);
+            if (best == 0.0) {
+                status = first_par + j + 1;
+            } else {
+#pragma unroll
+                for (int i = j + 1; i < kFastM; ++i) {
+                    if (i == p) {
+                        const double t = col[i];
+                        col[i] = col[j];
+                        col[j] = t;
+                    }
+                }
+                // Row i -= l_i * row j with l_i = a_ij / pivot, as in the LU
+                // (so an exactly dependent row cancels to an exact zero), then
+                // row j /= pivot.  l_i is the reciprocal product corrected once
+                // by its exact residual (Markstein's division step).
+                const double piv = lane_value(col[j], j);
+                const double inv = 1.0 / piv;
+#pragma unroll
+                for (int i = 0; i < kFastM; ++i) {
+                    if (i != j && i < m) {
+                        const double aij = lane_value(col[i], j);
+                        const double l0 = aij * inv;
+                        const double li = fma(fma(-l0, piv, aij), inv, l0);
+                        col[i] = fma(-li, col[j], col[i]);
+                    }
+                }
+                col[j] = col[j] / piv;
+            }
+        }
+    }
+    if (status == 0 && c >= 0 && c < k) {
+#pragma unroll
+        for (int r = 0; r < kFastM; ++r) sD[c * kFastLd + r] = col[r];
+    }
+    if (lane == 0) sm.status = status;
+}
+
+// One workgroup per (set, chunk): after the elimination its four waves copy
+// the systematic survivors, then combine the missing blocks on the matrix
+// cores; the workgroups resident on a compute unit drift apart in phase, so
+// copies and matrix-core work overlap across them.
+// KS: matrix-core K steps (4 survivors each) the kernel is built for, k <= 4 KS.
+template <int KS, int E, typename YT>
+__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
+                                                               int elems_per_block) {
+    __shared__ SetMeta sm;
+    __shared__ double sD[64 * kFastLd];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int k = a.k;
+    const int64_t b = blockIdx.x / chunks;
+    const int64_t chunk = blockIdx.x % chunks;
+    const bool writer = (chunk == 0 && tid == 0);
+    if (!setup_set(a, single, b, writer, sm)) return;
+    const int m = sm.m;
+    const int first_par = k - m;
+    if (m > 0 && wv == 0) eliminate_wave(a, sm, m, first_par, lane, sD);
+    __syncthreads();
+    if (sm.status != 0) {
+        if (writer) a.info[b] = sm.status;
+        return;
+    }
+    if (writer) a.info[b] = 0;
+
+    const YT* Y = static_cast<const YT*>(a.Y);
+    float* out = a.out + b * a.out_stride;
+    const int s = static_cast<int>(a.s);
+    const int total = static_cast<int>(a.qb * a.s);
+    const int e0 = static_cast<int>(chunk) * elems_per_block;
+    const int e1 = min(total, e0 + elems_per_block);
+    constexpr int kWaves = kThreads / 64;
+
+    // Systematic survivors: U survivors' loads in flight per thread
+    // (straight-line: a batch past the last survivor re-reads the last one
+    // and stores nothing).
+    constexpr int U = 8;
+    for (int e = e0 + E * tid; e < e1; e += E * kThreads) {
+        const int t = e / s, col = e - t * s;
+        const int64_t orow = static_cast<int64_t>(t) * a.ldo + col;
+        for (int c0 = 0; c0 < first_par; c0 += U) {
+            float v[U][E];
+#pragma unroll
+            for (int u = 0; u < U; ++u) load_f32<E, YT>(Y + sm.yoff[min(c0 + u, first_par - 1)] + e, v[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (c0 + u < first_par) {
+                    const int w = sm.S[c0 + u];
+                    if (t < sm.lim[w]) store_out<E>(a, out, sm.ooff[w] + orow, v[u]);
+                }
+            }
+        }
+    }
+    if (m == 0) return;
+
+    // Missing blocks: 16-element tiles, one wave per tile.  Lane (li, lk)
+    // holds D[li][4 st + lk] (A operand) and loads Y_{S[4 st + lk]}[e] (B);
+    // accumulator item v is out block M[4 v + lk], element li of the tile.
+    const int li = lane & 15, lk = lane >> 4;
+    double af[KS];
+    int32_t yo[KS];
+    uint32_t valid = 0;                   // bit st: survivor 4 st + lk exists
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+        const int c = 4 * st + lk;
+        af[st] = c < k ? sD[c * kFastLd + li] : 0.0;
+        yo[st] = c < k ? static_cast<int32_t>(sm.yoff[c]) : 0;
+        valid |= (c < k ? 1u : 0u) << st;
+    }
+    const int ntiles = (e1 - e0 + 15) / 16;
+    for (int tile = wv; tile < ntiles; tile += kWaves) {
+        const int e = e0 + tile * 16 + li;
+        // Straight-line loads, all issued before the first is used.  A lane
+        // past the chunk's end reads its last element instead: column li of
+        // the product depends on column li of Y only, and is not stored.
+        const int el = min(e, e1 - 1);
+        YT yv[KS];
+#pragma unroll
+        for (int st = 0; st < KS; ++st) yv[st] = Y[yo[st] + el];
+        f64x4v acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+            // padding steps (k not a multiple of 4) contribute exact zeros
+            const double bv = (valid >> st) & 1u ? static_cast<double>(yv[st]) : 0.0;
+            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], bv, acc, 0, 0, 0);
+        }
+        if (e < e1) {
+            const int t = e / s, col = e - t * s;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int bb = 4 * v + lk;
+                if (bb < m) {
+                    const int w = sm.miss[bb];
+                    const double val = acc[v];
+                    if (t < sm.lim[w]) store_out<1>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, &val);
+                }
+            }
+        }
+    }
+}
+
+// The fast path takes codes (not sets) by their largest possible m, so a set
+// decodes with the same arithmetic alone or in a batch.
+bool fast_path_ok(const DecodeArgs& a) {
+    const int mmax = std::min(a.k, a.n - a.k);
+    return mmax <= kFastM && a.k + mmax <= 64 && static_cast<int64_t>(a.n) * a.qb * a.s <= 0x7FFFFFFF;
+}
+
+template <int E>
+hipError_t launch_fast(const DecodeArgs& a, const DecodeSet& single, hipStream_t st) {
+    const int64_t total = a.qb * a.s;
+    const int64_t max_chunks = std::max<int64_t>(1, ceil_div(total, static_cast<int64_t>(kThreads) * E));
+    const int64_t want = std::max<int64_t>(1, ceil_div(2048, a.batch));
+    const int64_t per = ceil_div(ceil_div(std::max<int64_t>(total, 1), std::min(max_chunks, want)), 16) * 16;
+    const int64_t chunks = std::max<int64_t>(1, ceil_div(total, per));
+    const int64_t blocks = chunks * a.batch;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const int ksteps = (a.k + 3) / 4;
+    const dim3 grid(static_cast<unsigned>(blocks));
+    const int per32 = static_cast<int>(per);
+#define CODED_FAST(KS)                                                                                      \
+    do {                                                                                                    \
+        if (a.y_f64)                                                                                        \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, double>), grid, dim3(kThreads), 0, st, a, single, \
+                               chunks, per32);                                                              \
+        else                                                                                                \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, float>), grid, dim3(kThreads), 0, st, a, single,  \
+                               chunks, per32);                                                              \
+    } while (0)
+    if (ksteps <= 4) CODED_FAST(4);
+    else if (ksteps <= 8) CODED_FAST(8);
+    else if (ksteps <= 12) CODED_FAST(12);
+    else CODED_FAST(16);
+#undef CODED_FAST
+    return hipGetLastError();
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) % 16) == 0; }
 
 template <int PASS, int E>
@@ -331,6 +611,11 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax,
     if (a.qb * a.s > 0x7FFFFFFF) return hipErrorInvalidValue;
     DecodeSet s{};
     if (single) s = *single;
+    if (fast_path_ok(a)) {
+        const bool vec4 = a.s % 4 == 0 && a.ldo % 4 == 0 && aligned16(a.out) && aligned16(a.Y) &&
+                          (a.batch == 1 || a.out_stride % 4 == 0) && (a.c == nullptr || aligned16(a.c));
+        return vec4 ? launch_fast<4>(a, s, st) : launch_fast<1>(a, s, st);
+    }
     const int rows = (std::max(mmax, 1) + 1) / 2 * 2;   // even: D pairs are read 16 bytes at a time
     if (mmax <= 2) return launch_p<2>(a, s, rows, st);
     if (mmax <= 4) return launch_p<4>(a, s, rows, st);
