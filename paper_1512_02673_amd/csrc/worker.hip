@@ -216,11 +216,11 @@ hipError_t launch_gemv_wg(const WorkerArgs& a, hipStream_t st) {
 
 template <int XR>
 hipError_t launch_gemv_t(const WorkerArgs& a, hipStream_t st) {
-    // Four rows per workgroup unless that leaves too few workgroups to fill
-    // the chip (256 CUs); then fewer.
+    // Four rows per workgroup (x is read once per four rows) unless that
+    // leaves fewer than four workgroups per compute unit (256 CUs); then fewer.
     const int64_t workers = a.n_sys + a.n_par;
-    if (ceil_div(a.qb, 4) * workers >= 4096) return launch_gemv_wg<4, XR>(a, st);
-    if (ceil_div(a.qb, 2) * workers >= 4096) return launch_gemv_wg<2, XR>(a, st);
+    if (ceil_div(a.qb, 4) * workers >= 1024) return launch_gemv_wg<4, XR>(a, st);
+    if (ceil_div(a.qb, 2) * workers >= 1024) return launch_gemv_wg<2, XR>(a, st);
     return launch_gemv_wg<1, XR>(a, st);
 }
 

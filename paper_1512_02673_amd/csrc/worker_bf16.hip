@@ -3,6 +3,8 @@
 // matrix-core kernel serves aligned shapes given a workspace; a vector kernel
 // serves the rest.
 #include "internal.h"
+#include <type_traits>
+
 #include "worker_common.h"
 
 namespace coded {
@@ -102,27 +104,27 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
         tile = (g - npar) % tiles;
         parity = false;
     }
-    const int nplanes = parity ? a.planes : 1;
     const int64_t plane = static_cast<int64_t>(a.n - a.k) * a.qb * a.r;
     const uint16_t* XT = static_cast<const uint16_t*>(a.xt);
     const int64_t ncols = min<int64_t>(16 * NTILE, a.s - c0);
+    // Every load in the K loop is unconditional, which lets the loads of a
+    // chunk and the next chunk's X^T all be in flight together (a load under
+    // a condition makes the compiler wait for everything in flight first).
+    // A padding row (past the block, or a systematic row past A) reads a
+    // clamped valid row instead: row i of the product depends on row i of
+    // the block only, and such rows are stored as zeros or not at all.
     const uint16_t* rp[SLABS][2];
     int64_t trow[SLABS];
 #pragma unroll
     for (int sl = 0; sl < SLABS; ++sl) {
         trow[sl] = tile * ROWS + (wv * SLABS + sl) * 16;
-        const int64_t t = trow[sl] + li;
-        rp[sl][0] = rp[sl][1] = nullptr;
-        if (t < a.qb) {
-            if (!parity) {
-                const int64_t rr = static_cast<int64_t>(worker) * a.qb + t;
-                if (rr < a.q) rp[sl][0] = static_cast<const uint16_t*>(a.A) + rr * a.lda;
-            } else {
-                const uint16_t* base =
-                    static_cast<const uint16_t*>(a.parity) + (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
-                rp[sl][0] = base;
-                if (nplanes == 2) rp[sl][1] = base + plane;
-            }
+        const int64_t t = min<int64_t>(trow[sl] + li, a.qb - 1);
+        if (!parity) {
+            const int64_t rr = min<int64_t>(static_cast<int64_t>(worker) * a.qb + t, a.q - 1);
+            rp[sl][0] = rp[sl][1] = static_cast<const uint16_t*>(a.A) + rr * a.lda;
+        } else {
+            rp[sl][0] = static_cast<const uint16_t*>(a.parity) + (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
+            rp[sl][1] = rp[sl][0] + plane;
         }
     }
     f32x4_t acc[SLABS][NTILE];
@@ -130,65 +132,87 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
     for (int sl = 0; sl < SLABS; ++sl)
 #pragma unroll
         for (int j = 0; j < NTILE; ++j) acc[sl][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    const bf16x8 zero8 = __builtin_bit_cast(bf16x8, u32x4_t{0u, 0u, 0u, 0u});
 
     u32x4_t xr[XV];
+    // X^T from clamped addresses; out-of-range values are zeroed when they
+    // are stored to LDS, so tail columns of A meet zeros.
     auto xload = [&](int64_t kc) {
 #pragma unroll
         for (int i = 0; i < XV; ++i) {
             const int e = tid + kThreads * i;
             const int col = e / (kBK / 8), v = e % (kBK / 8);
             const int64_t k = kc + 8 * v;
-            xr[i] = (col < ncols && k < a.r) ? *reinterpret_cast<const u32x4_t*>(XT + (c0 + col) * a.r + k)
-                                             : u32x4_t{0u, 0u, 0u, 0u};
+            xr[i] = *reinterpret_cast<const u32x4_t*>(XT + (c0 + min<int64_t>(col, ncols - 1)) * a.r +
+                                                      min<int64_t>(k, a.r - 8));
         }
     };
-    auto xstore = [&](int buf) {
+    auto xstore = [&](int buf, int64_t kc) {
 #pragma unroll
         for (int i = 0; i < XV; ++i) {
             const int e = tid + kThreads * i;
             const int col = e / (kBK / 8), v = e % (kBK / 8);
-            if (col < 16 * NTILE) *reinterpret_cast<u32x4_t*>(&sXT[buf][col][8 * v]) = xr[i];
+            const bool ok = col < ncols && kc + 8 * v < a.r;
+            if (col < 16 * NTILE)
+                *reinterpret_cast<u32x4_t*>(&sXT[buf][col][8 * v]) = ok ? xr[i] : u32x4_t{0u, 0u, 0u, 0u};
         }
     };
-    xload(0);
-    xstore(0);
-    __syncthreads();
-    int buf = 0;
-    for (int64_t kc = 0; kc < a.r; kc += kBK) {
-        bf16x8 af[KS][SLABS][2];
+    // NPL planes per row (compile time, so the loop has no per-plane branch).
+    // The A fragments of chunk c + 1 are loaded while chunk c feeds the
+    // matrix cores (two register sets, used alternately).
+    auto sweep = [&](auto npl) {
+        constexpr int NPL = decltype(npl)::value;
+        bf16x8 fa[KS][SLABS][NPL], fb[KS][SLABS][NPL];
+        auto aload = [&](int64_t kc, bf16x8 (&af)[KS][SLABS][NPL]) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int64_t k = kc + 32 * ks + 8 * lk;
+            for (int ks = 0; ks < KS; ++ks) {
+                const int64_t k = min<int64_t>(kc + 32 * ks + 8 * lk, a.r - 8);
 #pragma unroll
-            for (int sl = 0; sl < SLABS; ++sl)
+                for (int sl = 0; sl < SLABS; ++sl)
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    af[ks][sl][h] = (rp[sl][h] && h < nplanes && k < a.r)
-                                        ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4_t*>(rp[sl][h] + k))
-                                        : zero8;
-        }
-        const bool more = kc + kBK < a.r;
-        if (more) xload(kc + kBK);
+                    for (int h = 0; h < NPL; ++h)
+                        af[ks][sl][h] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4_t*>(rp[sl][h] + k));
+            }
+        };
+        auto step = [&](int64_t kc, int buf, bf16x8 (&cur)[KS][SLABS][NPL], bf16x8 (&nxt)[KS][SLABS][NPL]) {
+            const bool more = kc + kBK < a.r;
+            if (more) {
+                xload(kc + kBK);
+                aload(kc + kBK, nxt);
+            }
+            // keep the scheduler from sinking these loads into the MFMA
+            // sequence (it would serialise them one at a time)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            bf16x8 bfr[NTILE];
+            for (int ks = 0; ks < KS; ++ks) {
+                bf16x8 bfr[NTILE];
 #pragma unroll
-            for (int j = 0; j < NTILE; ++j)
-                bfr[j] = *reinterpret_cast<const bf16x8*>(&sXT[buf][16 * j + li][32 * ks + 8 * lk]);
+                for (int j = 0; j < NTILE; ++j)
+                    bfr[j] = *reinterpret_cast<const bf16x8*>(&sXT[buf][16 * j + li][32 * ks + 8 * lk]);
 #pragma unroll
-            for (int sl = 0; sl < SLABS; ++sl)
+                for (int sl = 0; sl < SLABS; ++sl)
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    if (h < nplanes)
+                    for (int h = 0; h < NPL; ++h)
 #pragma unroll
                         for (int j = 0; j < NTILE; ++j)
-                            acc[sl][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ks][sl][h], bfr[j], acc[sl][j], 0, 0, 0);
-        }
-        if (more) xstore(buf ^ 1);
+                            acc[sl][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[ks][sl][h], bfr[j], acc[sl][j], 0, 0, 0);
+            }
+            if (more) xstore(buf ^ 1, kc + kBK);
+            __syncthreads();
+        };
+        xload(0);
+        aload(0, fa);
+        xstore(0, 0);
         __syncthreads();
-        buf ^= 1;
-    }
+        for (int64_t kc = 0; kc < a.r; kc += 2 * kBK) {
+            step(kc, 0, fa, fb);
+            if (kc + kBK < a.r) step(kc + kBK, 1, fb, fa);
+        }
+    };
+    if (parity && a.planes == 2)
+        sweep(std::integral_constant<int, 2>{});
+    else
+        sweep(std::integral_constant<int, 1>{});
+
     float* Y = static_cast<float*>(a.Y);
 #pragma unroll
     for (int sl = 0; sl < SLABS; ++sl)
@@ -198,7 +222,10 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_mfma_kernel(WorkerArgs a, 
             for (int v = 0; v < 4; ++v) {
                 const int64_t t = trow[sl] + 4 * lk + v;
                 const int64_t col = 16 * j + li;
-                if (t < a.qb && col < ncols) Y[(static_cast<int64_t>(worker) * a.qb + t) * a.s + c0 + col] = acc[sl][j][v];
+                // systematic rows past A are the zero padding of the last block
+                const bool inside = parity || static_cast<int64_t>(worker) * a.qb + t < a.q;
+                if (t < a.qb && col < ncols)
+                    Y[(static_cast<int64_t>(worker) * a.qb + t) * a.s + c0 + col] = inside ? acc[sl][j][v] : 0.0f;
             }
 }
 
