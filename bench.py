@@ -562,6 +562,81 @@ def runtime_sim_workload(args):
     return result
 
 
+def harmonic(n: int) -> float:
+    return float(sum(1.0 / i for i in range(1, n + 1)))
+
+
+def straggler_workload(args):
+    """Real straggling on the GEMV workload's data: the protocol of Sec. III-A
+    against the clock.  Each worker's product is started at its drawn task
+    time T_i (Sec. III-C, eq. shifted_exp, shift 1, rate 1) times a time unit;
+    the decode starts when the first k products have completed, and workers
+    not started by then never run.  The same draws are run with the (16,12)
+    code and uncoded (the (16,16) identity code: every one of 16 workers must
+    finish).  The runtime model predicts E[T_(12 of 16)] = (1 + H_16 - H_4)/12
+    and E[T_(16 of 16)] = (1 + H_16)/16 (eqs. mds_coded, uncoded); the
+    measured latency adds the products, the decode and the host's polling.
+    One step is one coded and one uncoded product."""
+    import torch
+
+    from paper_1512_02673_amd import binding as lib
+
+    w = synth.WORKLOADS["gemv16x12_65536x8192"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    D, W, unit = args.steps, args.warmup, args.time_unit_us
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    P = synth.parity_matrix(n, k, seed)
+    x = synth.gaussian((r,), seed, synth.STREAM_X, 0)
+    coded = lib.Code.systematic(P, planes=2)
+    uncoded = lib.Code.systematic(np.zeros((0, n)), planes=2)
+    dA, dx = torch.from_numpy(A).cuda(), torch.from_numpy(x).cuda()
+    par = lib.alloc_parity(coded, q, r, torch.float32)
+    lib.coded_encode(coded, dA, par)
+    Yc, Yu = lib.alloc_y(coded, q, 1, torch.float64), lib.alloc_y(uncoded, q, 1, torch.float64)
+    out = torch.empty(q, dtype=torch.float32, device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    def run(code, Y, parity, draw):
+        surv, tl, lat = lib.coded_straggler_matmul(code, dA, parity, dx, Y, out, info, seed, draw, unit)
+        if int(info.item()) != 0:
+            raise RuntimeError("a straggler decode reported a singular or invalid survivor set")
+        return surv, tl, lat
+
+    for d in range(W):
+        run(coded, Yc, par, (1 << 30) + d)
+        run(uncoded, Yu, None, (1 << 30) + d)
+    lat_c, lat_u, over_c, over_u, started = [], [], [], [], []
+    t0 = time.perf_counter()
+    for d in range(D):
+        surv, tl, lat = run(coded, Yc, par, d)
+        lat_c.append(lat)
+        over_c.append(lat - np.sort(tl[:, 0])[k - 1])
+        started.append(int(np.sum(tl[:, 1] >= 0)))
+        surv, tl, lat = run(uncoded, Yu, None, d)
+        lat_u.append(lat)
+        over_u.append(lat - np.max(tl[:, 0]))
+    elapsed = time.perf_counter() - t0
+    model_c = (1.0 + harmonic(n) - harmonic(n - k)) / k * unit * 1e-3
+    model_u = (1.0 + harmonic(n)) / n * unit * 1e-3
+    mc, mu = float(np.mean(lat_c)) * 1e-3, float(np.mean(lat_u)) * 1e-3
+    return {
+        "metric": METRIC, "value": mc, "unit": "ms per coded product (mean latency under straggling)",
+        "n_gpus": 1, "steps": D, "warmup": W, "ms_per_step": elapsed * 1e3 / D, "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "straggler16x12_65536x8192", "n": n, "k": k, "q": q, "r": r,
+                   "time_unit_us": unit, "shift": 1.0, "rate": 1.0, "survivors_only": True},
+        "uncoded_ms": mu, "speedup_vs_uncoded": mu / mc,
+        "model": {"coded_ms": model_c, "uncoded_ms": model_u, "speedup": model_u / model_c},
+        "overhead_ms": {"coded_mean": float(np.mean(over_c)) * 1e-3, "uncoded_mean": float(np.mean(over_u)) * 1e-3,
+                        "note": "latency minus the draw's own k-th (or last) start time: products, decode, polling"},
+        "p95_ms": {"coded": float(np.percentile(lat_c, 95)) * 1e-3, "uncoded": float(np.percentile(lat_u, 95)) * 1e-3},
+        "workers_started_mean": float(np.mean(started)),
+        "roofline": None,
+        "roofline_note": "a latency experiment: the time is set by the injected runtimes, not by a kernel's roofline",
+    }
+
+
 def calibrate_copy(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -580,12 +655,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
                     choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8", "gd20x16_262144x4096",
-                             "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5"])
+                             "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
+                             "straggler16x12_65536x8192"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-products", type=int, default=300)
     ap.add_argument("--cpu-decodes", type=int, default=1000)
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--time-unit-us", type=float, default=10000.0,
+                    help="straggler workload: microseconds per unit of the runtime model")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the coded product is simulated on a single device); "
@@ -618,6 +696,12 @@ def main():
         if "--warmup" not in sys.argv:
             args.warmup = 2
         result = runtime_sim_workload(args)
+    elif args.workload == "straggler16x12_65536x8192":
+        if "--steps" not in sys.argv:
+            args.steps = 100
+        if "--warmup" not in sys.argv:
+            args.warmup = 3
+        result = straggler_workload(args)
     elif args.workload == "gd20x16_262144x4096":
         if "--steps" not in sys.argv:
             args.steps = 200

@@ -217,6 +217,43 @@ coded_status coded_matmul(const coded_code* code, coded_dtype dt, const void* A,
                           float* out, int64_t ldo, void* workspace, int32_t* info, void* stream);
 
 /*
+ * coded_straggler_matmul -- one coded product with real, timed straggling:
+ * the master/worker protocol of Sec. III-A run against the clock, with the
+ * worker runtimes of Sec. III-B/C (eq. shifted_exp) as start delays.
+ * Worker i's task time T_i = (shift - ln U_i / rate) / k comes from the same
+ * SplitMix64 word as coded_draw_survivors.  At T_i * time_unit_us
+ * microseconds after the call begins the host enqueues worker i's product
+ * (on one of four internal default-priority streams, after the work already
+ * on `stream`) and an event behind it.  The host polls the events: the first
+ * k products seen complete are the survivors, in arrival order, and the
+ * decode is enqueued on `stream` when the k-th arrives.  Then the other
+ * workers are started at once (launch_all != 0) or never (launch_all == 0:
+ * only the workers started before the k-th arrival compute).  The call
+ * returns when the decode has completed, so it blocks the host; work
+ * enqueued on `stream` afterwards waits for every product it started.
+ *   dt, A, parity, X, s, ldx   as coded_worker_mm; parity must be ready.
+ *   Y          device n x qb x s of y_dt (as coded_worker_mm); rows of
+ *              workers that do not run are left untouched.
+ *   workspace  coded_sizes' worker_workspace_bytes (BF16: required).
+ *   out, ldo, info   as coded_decode.
+ *   survivors_out  host int32[k] or NULL: the survivors in arrival order.
+ *   timeline_out   host double[3 n] or NULL: for worker i, [3i] its start
+ *              time, [3i+1] when it was enqueued, [3i+2] when the host saw it
+ *              complete, in microseconds from the call's start (-1: not
+ *              enqueued, or not seen complete before the decode).
+ *   latency_us_out host double or NULL: call start to decode complete.
+ * Requires rate > 0, time_unit_us >= 0 and a k-th start time under 60 s.
+ * Calls with the same code object must not overlap (the internal streams
+ * and events belong to the code).
+ */
+coded_status coded_straggler_matmul(coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r,
+                                    int64_t lda, const void* parity, const void* X, int64_t s, int64_t ldx,
+                                    uint64_t seed, uint64_t draw, double shift, double rate, double time_unit_us,
+                                    int32_t launch_all, void* Y, coded_dtype y_dt, void* workspace, float* out,
+                                    int64_t ldo, int32_t* info, int32_t* survivors_out, double* timeline_out,
+                                    double* latency_us_out, void* stream);
+
+/*
  * coded_transpose -- AT = A^T for fp32 A (q x r, row stride lda) into AT
  * (r x q, row stride ldat >= q).  This forms the column split of A that the
  * transposed code of coded gradient descent encodes (Sec. III-E: worker i

@@ -39,6 +39,9 @@ _SIGNATURES = {
     "coded_draw_survivor_sets": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_i32, _c_i32, _c_p, _c_p]),
     "coded_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i32, _c_p, _c_i64, _c_i64,
                               _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_straggler_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64,
+                                        _c_u64, _c_u64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_p, _c_i32, _c_p, _c_p,
+                                        _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "coded_transpose": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i64, _c_p]),
     "coded_gd_sizes": (_c_i32, [_c_p, _c_p, _c_i64, _c_i64, _c_p]),
     "coded_gd_step": (_c_i32, [_c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_dbl,
@@ -277,6 +280,31 @@ def coded_matmul(code: Code, A, parity, X, out, workspace, info, seed: int, draw
                               _ptr(X), s, ldx, seed, draw, shift, rate, surv.ctypes.data_as(ctypes.c_void_p),
                               ctypes.addressof(t), _ptr(out), ldo, _ptr(workspace), _ptr(info), _stream(stream)))
     return surv, t.value
+
+
+def coded_straggler_matmul(code: Code, A, parity, X, Y, out, info, seed: int, draw: int, time_unit_us: float,
+                           launch_all: bool = False, workspace="auto", shift: float = 1.0, rate: float = 1.0,
+                           stream=None):
+    """One coded product with real, timed straggling (blocks until the decode is done).
+    Returns (survivors int32[k] in arrival order, timeline float64[n, 3] in microseconds:
+    start time, enqueue time, completion seen, -1 where it did not happen, latency in microseconds)."""
+    q, r, lda = _matrix(A, "A")
+    rx, s, ldx = _matrix(X, "X")
+    if rx != r:
+        raise ValueError("X must have r rows")
+    _, so, ldo = _matrix(out, "out")
+    if isinstance(workspace, str):
+        workspace = worker_workspace(code, A, X)
+    surv = np.zeros(code.k, dtype=np.int32)
+    timeline = np.zeros((code.n, 3), dtype=np.float64)
+    lat = ctypes.c_double()
+    _check(lib().coded_straggler_matmul(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _ptr(X), s,
+                                        ldx, seed, draw, shift, rate, time_unit_us, int(bool(launch_all)), _ptr(Y),
+                                        _dtype_code(Y), _ptr(workspace), _ptr(out), ldo, _ptr(info),
+                                        surv.ctypes.data_as(ctypes.c_void_p),
+                                        timeline.ctypes.data_as(ctypes.c_void_p), ctypes.addressof(lat),
+                                        _stream(stream)))
+    return surv, timeline, lat.value
 
 
 def coded_transpose(A, AT, stream=None) -> None:

@@ -2,12 +2,14 @@
 // objects, survivor draws and kernel launches.  Every entry point validates
 // on the host before enqueueing anything and never throws.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstring>
 #include <exception>
 #include <new>
 #include <set>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "internal.h"
@@ -111,7 +113,7 @@ coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64
 
 coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                         const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* mask, void* Y,
-                        coded_dtype y_dt, void* workspace, hipStream_t st) {
+                        coded_dtype y_dt, void* workspace, hipStream_t st, bool xt_ready = false) {
     if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
     if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
     if (s == 1 && ldx != 1 && dt == CODED_F32) {
@@ -142,6 +144,7 @@ coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int6
     a.planes = c->planes;
     a.y_f64 = y_dt == CODED_F64;
     a.xt = dt == CODED_BF16 ? workspace : nullptr;
+    a.xt_ready = xt_ready ? 1 : 0;
     for (int i = 0; i < c->n; ++i) {
         if (mask && !mask[i]) continue;
         if (i < c->k)
@@ -235,6 +238,9 @@ coded_status coded_code_destroy(coded_code* c) {
     CODED_GUARD_BEGIN
     if (!c) return CODED_OK;
     hipError_t e = hipSuccess;
+    for (hipEvent_t ev : c->worker_events) hipEventDestroy(ev);
+    if (c->start_event) hipEventDestroy(c->start_event);
+    for (hipStream_t w : c->worker_streams) hipStreamDestroy(w);
     if (c->dG) e = hipFree(c->dG);
     delete c;
     if (e != hipSuccess) return hip_fail(e, "coded_code_destroy");
@@ -403,6 +409,184 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     if (coded_status s2 = do_decode_single(c, set, m, workspace, y_dt, q, s, out, ldo, info, st)) return s2;
     if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
     if (t_overall_out) *t_overall_out = t;
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+namespace {
+
+constexpr int kStragglerStreams = 4;          // the device's default number of hardware queues
+constexpr double kStragglerMaxStartUs = 60e6;  // latest start the host waits for
+
+coded_status ensure_straggler_state(coded_code* c) {
+    if (!c->worker_streams.empty()) return CODED_OK;
+    std::vector<hipStream_t> streams;
+    std::vector<hipEvent_t> events;
+    hipEvent_t start = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&start, hipEventDisableTiming);
+    for (int i = 0; e == hipSuccess && i < kStragglerStreams; ++i) {
+        hipStream_t w = nullptr;
+        e = hipStreamCreateWithFlags(&w, hipStreamNonBlocking);
+        if (e == hipSuccess) streams.push_back(w);
+    }
+    for (int i = 0; e == hipSuccess && i < c->n; ++i) {
+        hipEvent_t ev = nullptr;
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e == hipSuccess) events.push_back(ev);
+    }
+    if (e != hipSuccess) {
+        for (hipEvent_t ev : events) hipEventDestroy(ev);
+        for (hipStream_t w : streams) hipStreamDestroy(w);
+        if (start) hipEventDestroy(start);
+        return hip_fail(e, "straggler streams and events");
+    }
+    c->worker_streams = std::move(streams);
+    c->worker_events = std::move(events);
+    c->start_event = start;
+    return CODED_OK;
+}
+
+}  // namespace
+
+coded_status coded_straggler_matmul(coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                                    const void* parity, const void* X, int64_t s, int64_t ldx, uint64_t seed,
+                                    uint64_t draw, double shift, double rate, double time_unit_us,
+                                    int32_t launch_all, void* Y, coded_dtype y_dt, void* workspace, float* out,
+                                    int64_t ldo, int32_t* info, int32_t* survivors_out, double* timeline_out,
+                                    double* latency_us_out, void* stream) {
+    CODED_GUARD_BEGIN
+    using clock = std::chrono::steady_clock;
+    const auto t0 = clock::now();
+    auto now_us = [&]() { return std::chrono::duration<double, std::micro>(clock::now() - t0).count(); };
+    if (coded_status st = check_code(c)) return st;
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
+    if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
+    if (s == 1 && ldx != 1 && dt == CODED_F32) return fail(CODED_ERR_UNSUPPORTED, "s == 1 needs ldx == 1");
+    if (ldo < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldo must be >= max(s, 1)");
+    if (!info) return fail(CODED_ERR_ARG, "info is NULL");
+    if (!(rate > 0.0) || !std::isfinite(shift)) return fail(CODED_ERR_ARG, "need rate > 0 and a finite shift");
+    if (!(time_unit_us >= 0.0) || !std::isfinite(time_unit_us)) return fail(CODED_ERR_ARG, "need time_unit_us >= 0");
+    if (draw >= (1ull << 40)) return fail(CODED_ERR_ARG, "draw must be < 2^40");
+    const int64_t qb = block_rows(q, c->k);
+    if (qb * s > 0 && (!Y || !out)) return fail(CODED_ERR_ARG, "Y or out is NULL");
+    if (qb * s > 0 && r > 0 && (!X || (q > 0 && !A) || (!parity && c->n > c->k)))
+        return fail(CODED_ERR_ARG, "A, parity or X is NULL");
+    if (dt == CODED_BF16 && qb * s > 0 && r > 0 && !workspace)
+        return fail(CODED_ERR_ARG, "bf16 needs the worker workspace");
+    if (decode_lds_bytes(c->k, std::max(std::min(c->k, c->n - c->k), 1)) > kMaxDecodeLds)
+        return fail(CODED_ERR_UNSUPPORTED, "survivor system too large for one workgroup's LDS");
+
+    // Start times from the runtime model (Sec. III-C), in the order they fall.
+    const int n = c->n, k = c->k;
+    std::vector<double> sched(n);
+    coded_rng::worker_times(n, k, seed, draw, shift, rate, sched.data());
+    for (double& t : sched) t *= time_unit_us;
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return sched[a] < sched[b]; });
+    if (sched[order[k - 1]] > kStragglerMaxStartUs)
+        return fail(CODED_ERR_ARG, "the k-th start time exceeds 60 s; use a smaller time unit");
+    if (coded_status st = ensure_straggler_state(c)) return st;
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    if (dt == CODED_BF16 && qb * s > 0 && r > 0) {
+        // X is transposed once, before any worker starts (the workers share it)
+        WorkerArgs xa{};
+        xa.X = X;
+        xa.r = r;
+        xa.s = s;
+        xa.ldx = ldx;
+        xa.xt = workspace;
+        e = launch_transpose_x_bf16(xa, st);
+        if (e != hipSuccess) return hip_fail(e, "transpose launch");
+    }
+    // Products start after everything already enqueued on the caller's stream.
+    e = hipEventRecord(c->start_event, st);
+    for (int i = 0; e == hipSuccess && i < kStragglerStreams; ++i) e = hipStreamWaitEvent(c->worker_streams[i], c->start_event, 0);
+    if (e != hipSuccess) return hip_fail(e, "ordering the worker streams");
+
+    std::vector<double> launched_at(n, -1.0), seen_at(n, -1.0);
+    std::vector<int> pending, arrivals;
+    std::vector<uint8_t> mask(n, 0);
+    int next = 0, launches = 0;
+    auto launch = [&](int i) -> coded_status {
+        std::fill(mask.begin(), mask.end(), 0);
+        mask[i] = 1;
+        hipStream_t ws = c->worker_streams[launches % kStragglerStreams];
+        launched_at[i] = now_us();
+        if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, mask.data(), Y, y_dt, workspace, ws,
+                                         dt == CODED_BF16))
+            return s2;
+        hipError_t e2 = hipEventRecord(c->worker_events[i], ws);
+        if (e2 != hipSuccess) return hip_fail(e2, "worker event");
+        ++launches;
+        pending.push_back(i);
+        return CODED_OK;
+    };
+    // The master's loop: start the workers whose time has come, collect
+    // completions, stop at the k-th.
+    while (static_cast<int>(arrivals.size()) < k) {
+        const double t = now_us();
+        while (next < n && sched[order[next]] <= t)
+            if (coded_status s2 = launch(order[next++])) return s2;
+        for (size_t j = 0; j < pending.size();) {
+            const int i = pending[j];
+            const hipError_t qe = hipEventQuery(c->worker_events[i]);
+            if (qe == hipSuccess) {
+                seen_at[i] = now_us();
+                arrivals.push_back(i);
+                pending.erase(pending.begin() + j);
+            } else if (qe == hipErrorNotReady) {
+                ++j;
+            } else {
+                return hip_fail(qe, "worker event query");
+            }
+        }
+        if (static_cast<int>(arrivals.size()) >= k) break;
+        if (t > kStragglerMaxStartUs + 60e6) return fail(CODED_ERR_HIP, "workers did not complete within 60 s");
+        // sleep through long gaps before the next start, poll otherwise
+        const double gap = next < n ? sched[order[next]] - now_us() : 0.0;
+        if (pending.empty() && gap > 300.0)
+            std::this_thread::sleep_for(std::chrono::microseconds(static_cast<int64_t>(std::min(gap - 200.0, 1000.0))));
+        else
+            std::this_thread::yield();
+    }
+    arrivals.resize(k);
+
+    // Decode from the first k arrivals, in arrival order.
+    DecodeSet set;
+    int m = 0;
+    if (coded_status s2 = take_survivors(c, arrivals.data(), k, set, m)) return s2;
+    for (int i : arrivals) {
+        e = hipStreamWaitEvent(st, c->worker_events[i], 0);
+        if (e != hipSuccess) return hip_fail(e, "ordering the decode");
+    }
+    if (coded_status s2 = do_decode_single(c, set, m, Y, y_dt, q, s, out, ldo, info, st)) return s2;
+    e = hipEventRecord(c->start_event, st);     // reused: marks the decode's end
+    if (e != hipSuccess) return hip_fail(e, "decode event");
+    // The rest of the workers: started now (launch_all) or never (survivors only).
+    if (launch_all)
+        while (next < n)
+            if (coded_status s2 = launch(order[next++])) return s2;
+    e = hipEventSynchronize(c->start_event);
+    if (e != hipSuccess) return hip_fail(e, "decode wait");
+    const double latency = now_us();
+    // Later work on the caller's stream waits for every product started here.
+    for (int i : pending) {
+        e = hipStreamWaitEvent(st, c->worker_events[i], 0);
+        if (e != hipSuccess) return hip_fail(e, "ordering the stragglers");
+    }
+    if (survivors_out) std::copy(arrivals.begin(), arrivals.end(), survivors_out);
+    if (latency_us_out) *latency_us_out = latency;
+    if (timeline_out)
+        for (int i = 0; i < n; ++i) {
+            timeline_out[3 * i] = sched[i];
+            timeline_out[3 * i + 1] = launched_at[i];
+            timeline_out[3 * i + 2] = seen_at[i];
+        }
     return CODED_OK;
     CODED_GUARD_END
 }

@@ -14,6 +14,12 @@ struct coded_code {
     std::vector<double> G;     // host copy, n*k row-major
     double* dG = nullptr;      // device copy, n*k row-major
     int device = 0;
+    // Created on first use by coded_straggler_matmul, released with the code:
+    // default-priority streams the worker products run on, one completion
+    // event per worker, and an event that orders them after the caller.
+    std::vector<hipStream_t> worker_streams;
+    std::vector<hipEvent_t> worker_events;
+    hipEvent_t start_event = nullptr;
 };
 
 namespace coded {
@@ -48,11 +54,14 @@ struct WorkerArgs {
     int32_t y_f64;        // 1: Y is fp64, 0: Y is fp32
     int32_t n_sys, n_par; // active systematic / parity workers
     void* xt;             // bf16 only: scratch for X transposed (s x r), or null
+    int32_t xt_ready;     // bf16 only: xt already holds X transposed (skip the transpose)
     uint8_t sys_ids[kMaxN];
     uint8_t par_ids[kMaxN];
 };
 hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st);
 hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
+// bf16: X (r x s, row stride ldx) transposed into a.xt.
+hipError_t launch_transpose_x_bf16(const WorkerArgs& a, hipStream_t st);
 // Bytes of the bf16 worker workspace (X transposed), 256-byte aligned.
 int64_t worker_workspace_bytes_bf16(int64_t r, int64_t s);
 
@@ -96,6 +105,8 @@ uint64_t splitmix64_output(uint64_t seed, uint64_t index);
 uint64_t runtime_word(uint64_t seed, uint64_t stream, uint64_t draw, uint64_t worker);
 // Survivors of one draw: k worker indices ascending; returns T_(k).
 double draw_survivors(int n, int k, uint64_t seed, uint64_t draw, double shift, double rate, int32_t* out);
+// Task times of the n workers of one draw: t[i] = (shift - ln U_i / rate) / k.
+void worker_times(int n, int k, uint64_t seed, uint64_t draw, double shift, double rate, double* t);
 // W_{-1}(x) for -1/e <= x < 0 (lower real branch of Lambert W).
 double lambert_w_lower(double x);
 }  // namespace coded_rng

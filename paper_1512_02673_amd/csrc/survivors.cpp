@@ -51,6 +51,14 @@ double draw_survivors(int n, int k, uint64_t seed, uint64_t draw, double shift, 
     return (shift + (-std::log(u)) / rate) / static_cast<double>(k);
 }
 
+void worker_times(int n, int k, uint64_t seed, uint64_t draw, double shift, double rate, double* t) {
+    for (int i = 0; i < n; ++i) {
+        const uint64_t w = runtime_word(seed, kRuntimeStream, draw, static_cast<uint64_t>(i));
+        const double u = (static_cast<double>(w >> 11) + 0.5) * 0x1.0p-53;
+        t[i] = (shift + (-std::log(u)) / rate) / static_cast<double>(k);
+    }
+}
+
 double lambert_w_lower(double x) {
     // Halley's iteration on f(w) = w e^w - x, started from the branch-point
     // series near -1/e or from the asymptotic logarithmic form near 0.

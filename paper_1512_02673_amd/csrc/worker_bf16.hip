@@ -262,15 +262,20 @@ hipError_t launch_waves(K kernel, const WorkerArgs& a, int64_t wsys, int64_t wpa
 
 int64_t worker_workspace_bytes_bf16(int64_t r, int64_t s) { return (r * s * 2 + 255) / 256 * 256; }
 
+hipError_t launch_transpose_x_bf16(const WorkerArgs& a, hipStream_t st) {
+    if (a.r == 0 || a.s == 0) return hipSuccess;
+    const int64_t tr = ceil_div(a.r, 64), ts = ceil_div(a.s, 64);
+    hipLaunchKernelGGL(transpose_x_bf16_kernel, dim3(static_cast<unsigned>(tr * ts)), dim3(256), 0, st,
+                       static_cast<const uint16_t*>(a.X), a.r, a.s, a.ldx, static_cast<uint16_t*>(a.xt), ts);
+    return hipGetLastError();
+}
+
 hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st) {
     if (a.qb == 0 || a.s == 0) return hipSuccess;
     const bool mfma = a.xt != nullptr && a.r > 0 && a.r % 8 == 0 && a.lda % 8 == 0 && aligned(a.A, 16) &&
                       (a.parity == nullptr || aligned(a.parity, 16)) && aligned(a.xt, 16);
     if (!mfma) return launch_waves(gemm_small_bf16_kernel<4>, a, a.qb, a.qb, st);
-    const int64_t tr = ceil_div(a.r, 64), ts = ceil_div(a.s, 64);
-    hipLaunchKernelGGL(transpose_x_bf16_kernel, dim3(static_cast<unsigned>(tr * ts)), dim3(256), 0, st,
-                       static_cast<const uint16_t*>(a.X), a.r, a.s, a.ldx, static_cast<uint16_t*>(a.xt), ts);
-    hipError_t e = hipGetLastError();
+    hipError_t e = a.xt_ready ? hipSuccess : launch_transpose_x_bf16(a, st);
     if (e != hipSuccess) return e;
     constexpr int SLABS = 2, ROWS = kWaves * SLABS * 16;
     const int64_t tiles = ceil_div(a.qb, ROWS);

@@ -74,6 +74,8 @@ def test_host_argument_errors(lib):
         lib.CODED_ERR_ARG
     assert h.coded_encode(None, 0, None, 0, 0, 1, None, None) == lib.CODED_ERR_ARG
     assert h.coded_decode(None, None, 0, None, 2, 0, 0, None, 1, None, None) == lib.CODED_ERR_ARG
+    assert h.coded_straggler_matmul(None, 0, None, 0, 0, 1, None, None, 1, 1, 0, 0, 1.0, 1.0, 1.0, 0, None, 2, None,
+                                    None, 1, None, None, None, None, None) == lib.CODED_ERR_ARG
 
 
 @pytest.mark.parametrize("n,mu", [(10, 1.0), (100, 0.5), (1000, 1.0), (64, 2.0), (7, 0.1)])
