@@ -54,6 +54,8 @@ def measured_traffic(per_launch_algorithmic: float):
         return None
     if t.get("kernel_source_sha256") != kernel_source_hash():
         return None
+    if abs(float(t.get("algorithmic_bytes_per_launch", -1.0)) - per_launch_algorithmic) > 1.0:
+        return None                      # counters of another launch shape
     return float(t["hbm_bytes_per_launch"])
 
 
@@ -73,16 +75,21 @@ def gemv_workload(args):
 
     from paper_1512_02673_amd import binding as lib
 
-    w = synth.WORKLOADS["gemv16x12_65536x8192"]
+    w = synth.WORKLOADS[args.workload if args.workload.startswith("gemv16x12") else "gemv16x12_65536x8192"]
     n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
     K, W = args.steps, args.warmup
     t0 = time.time()
     A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
-    P = synth.parity_matrix(n, k, seed)
+    if "parity_candidate" in w.extra:
+        # the certified generator (worst decode condition number over every survivor set)
+        P = synth.conditioned_parity_matrix(n, k, seed, w.extra["candidates"], pick=w.extra["parity_candidate"])[0]
+    else:
+        P = synth.parity_matrix(n, k, seed)
+    planes = w.extra.get("planes", 2)
     xs = np.stack([synth.gaussian((r,), seed, synth.STREAM_X, t) for t in range(K + W)])
     print(f"[bench] inputs drawn in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
 
-    code = lib.Code.systematic(P, planes=2)
+    code = lib.Code.systematic(P, planes=planes)
     dA = torch.from_numpy(A).cuda()
     dX = torch.from_numpy(xs).cuda()
     par = lib.alloc_parity(code, q, r, torch.float32)
@@ -654,7 +661,8 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
-                    choices=["gemv16x12_65536x8192", "decode64x48_16384x4096x8", "gd20x16_262144x4096",
+                    choices=["gemv16x12_65536x8192", "gemv16x12_conditioned_65536x8192",
+                             "decode64x48_16384x4096x8", "gd20x16_262144x4096",
                              "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
                              "straggler16x12_65536x8192"])
     ap.add_argument("--no-cpu-baseline", action="store_true")

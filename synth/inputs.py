@@ -7,6 +7,7 @@ here encodes, multiplies or decodes.
 from __future__ import annotations
 
 import concurrent.futures as _cf
+import itertools
 import os
 
 import numpy as np
@@ -117,3 +118,43 @@ def parity_matrix(n: int, k: int, seed: int, stream: int = STREAM_P, dtype: str 
 def integer_parity_matrix(n: int, k: int, seed: int, stream: int = STREAM_P, lo: int = -2, hi: int = 2) -> np.ndarray:
     """(n-k) x k float64 array of small integers (exact encode in fp32/bf16)."""
     return integers((n - k, k), seed, stream, lo=lo, hi=hi).astype(np.float64)
+
+
+def worst_decode_condition(P: np.ndarray) -> float:
+    """Largest 2-norm condition number over every square sub-block of P.
+
+    For a systematic code G = [I_k; P] the decode system of a survivor set is
+    the sub-block of P on the parity survivors' rows and the missing
+    systematic blocks' columns, so this bounds every decode of the code.
+    The enumeration is exhaustive (sum over m of C(n-k, m) C(k, m) blocks),
+    meant for small codes.
+    """
+    p, k = P.shape
+    worst = 1.0
+    for m in range(1, p + 1):
+        cols = np.array(list(itertools.combinations(range(k), m)))
+        for rows in itertools.combinations(range(p), m):
+            sv = np.linalg.svd(P[list(rows)][:, cols].transpose(1, 0, 2), compute_uv=False)
+            worst = max(worst, float(np.max(sv[:, 0] / sv[:, -1])))
+    return worst
+
+
+def conditioned_parity_matrix(n: int, k: int, seed: int, candidates: int, stream: int = STREAM_P,
+                              dtype: str = "f32", pick: int | None = None):
+    """The best of `candidates` seeded N(0,1) parity matrices by worst decode
+    condition number (candidate c is drawn with key c and rounded to dtype).
+    With `pick`, only that candidate is drawn and certified.
+    Returns (P, candidate, worst condition number)."""
+    best = None
+    for c in ([pick] if pick is not None else range(candidates)):
+        P = gaussian((n - k, k), seed, stream, c)
+        if dtype == "bf16":
+            P = bf16_round(P)
+        elif dtype != "f32":
+            raise ValueError(dtype)
+        P = P.astype(np.float64)
+        w = worst_decode_condition(P)
+        if best is None or w < best[2]:
+            best = (P, c, w)
+    return best
+

@@ -492,3 +492,34 @@ def test_coded_gd_matches_oracle_iterates(lib, torch, q, r, n1, k1, n2, k2):
         assert np.all(info.cpu().numpy() == 0)
         xt = x.cpu().numpy().astype(np.float64)
         assert np.max(np.abs(xt - rec[t])) <= 1e-4 * np.max(np.abs(rec[t])), t
+
+
+def test_conditioned_generator_single_plane_every_survivor_set(lib, torch):
+    """One fp32 parity plane (no lo plane) with the certified (16,12) generator
+    of the GEMV regime: every one of the C(16,12) = 1820 survivor sets decodes
+    within the fp32 tolerance.  The plain seed-2 draw, whose worst decode
+    system is 6.8 times worse conditioned, does worse on its worst set."""
+    w = synth.WORKLOADS["gemv16x12_conditioned_65536x8192"]
+    n, k, q, r = w.n, w.k, 12000, 8192
+    Pc, _, _ = synth.conditioned_parity_matrix(n, k, w.seed, w.extra["candidates"], pick=w.extra["parity_candidate"])
+    A = synth.gaussian((q, r), 41, synth.STREAM_A)
+    x = synth.gaussian((r,), 41, synth.STREAM_X)
+    ref = oc.plain_product(A, x[:, None])[:, 0]
+    sets = np.array(list(itertools.combinations(range(n), k)), dtype=np.int32)
+    dA, dx, dsets = torch.from_numpy(A).cuda(), torch.from_numpy(x).cuda(), torch.from_numpy(sets).cuda()
+    worst = {}
+    for name, P in (("conditioned", Pc), ("plain", synth.parity_matrix(n, k, w.seed))):
+        code = lib.Code.systematic(P, 1)
+        par = lib.alloc_parity(code, q, r, torch.float32)
+        lib.coded_encode(code, dA, par)
+        Y = lib.alloc_y(code, q, 1, torch.float64)
+        lib.coded_worker_mm(code, dA, par, dx, Y)
+        out = torch.empty((len(sets), q), dtype=torch.float32, device="cuda")
+        info = info_tensor(torch, len(sets))
+        lib.coded_decode_batched(code, dsets, Y, q, out, info)
+        torch.cuda.synchronize()
+        assert np.all(info.cpu().numpy() == 0)
+        got = out.cpu().numpy()
+        worst[name] = float(np.max(np.max(np.abs(got - ref[None, :]), axis=1)) / np.max(np.abs(ref)))
+    assert worst["conditioned"] <= TOL_F32, worst
+    assert worst["plain"] > worst["conditioned"], worst

@@ -333,3 +333,27 @@ def test_coded_gd_tracks_plain_gd_and_reaches_least_squares():
         assert np.allclose(rec[t], x, rtol=1e-9, atol=1e-11), t
     x_ls = np.linalg.lstsq(A, y, rcond=None)[0]
     assert np.allclose(rec[-1], x_ls, rtol=1e-6, atol=1e-8)
+
+
+def test_conditioned_generator_certificate():
+    """The GEMV regime's conditioned generator: every one of the C(16,12) survivor
+    sets of G = [I; P] has a decode system (parity survivors x missing blocks)
+    with 2-norm condition number at most the recorded bound, checked here by
+    walking the survivor sets themselves (not the sub-blocks of P)."""
+    w = synth.WORKLOADS["gemv16x12_conditioned_65536x8192"]
+    P, c, worst = synth.conditioned_parity_matrix(w.n, w.k, w.seed, w.extra["candidates"],
+                                                  pick=w.extra["parity_candidate"])
+    assert c == w.extra["parity_candidate"] and abs(worst - w.extra["worst_condition"]) < 0.1
+    G = oc.systematic_generator(P)
+    k = w.k
+    seen = 0
+    for S in itertools.combinations(range(w.n), k):
+        par = [i for i in S if i >= k]
+        miss = [j for j in range(k) if j not in S]
+        if par:
+            kap = np.linalg.cond(G[np.array(par)][:, miss])
+            assert kap <= worst * (1 + 1e-9), S
+            seen = max(seen, kap)
+    assert abs(seen - worst) <= 1e-6 * worst           # the bound is attained
+    # and the plain seed-2 draw of the same workload is worse
+    assert synth.worst_decode_condition(synth.parity_matrix(w.n, w.k, w.seed)) > 4 * worst
