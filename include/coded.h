@@ -329,6 +329,70 @@ const char* coded_last_error(void);
 /* Library version string. */
 const char* coded_version(void);
 
+/* ---------------------------------------------------------------- coded shuffling
+ * Sec. IV: before every iteration the q data rows are partitioned at random
+ * among n workers (S_i, q/n rows each); worker i's cache C_i holds S_i and
+ * s - q/n other rows.  The master multicasts, for every worker group I with
+ * |I| >= 2, the sum over i in I of the rows A(S_i cap C~_{I - i}) (C~_J: the
+ * rows cached by exactly the workers of J), each list zero-padded to the
+ * longest (Algorithm 1); worker i recovers its rows by subtracting the other
+ * members' rows, which it caches.  The cache update rule keeps the new S_i
+ * and s - q/n rows drawn from the old cache minus S_i.
+ * Draws: counter-based SplitMix64 of `seed` -- the partition of iteration t
+ * ranks the rows by output number (8<<56 | t<<40 | row) and deals them out
+ * q/n at a time; the cache rule of iteration t keeps, for worker i, the rows
+ * with the smallest output number (9<<56 | t<<40 | row<<6 | i) (ties: lower
+ * row).  The first caches are that rule applied to the whole data set.
+ * The state and the plan are host objects; encode and decode run on the
+ * device over device copies of the plan's tables.
+ */
+typedef struct coded_shuffle coded_shuffle;
+
+/* n in [1, 64] workers, q rows (a multiple of n, below 2^31), cache_rows in
+ * [q/n, q]; draws the partition and the caches of iteration 0. */
+coded_status coded_shuffle_create(int32_t n, int64_t q, int64_t cache_rows, uint64_t seed, coded_shuffle** out);
+coded_status coded_shuffle_destroy(coded_shuffle* sh);
+
+/* The current iteration t, partition (host int32[q]: worker of each row) and
+ * cache signatures (host uint64[q]: bit i set when worker i caches the row);
+ * any output may be NULL. */
+coded_status coded_shuffle_state(const coded_shuffle* sh, int64_t* t, int32_t* assign, uint64_t* cache_sig);
+
+/* Draws the partition of iteration t+1 and plans its transmission (replacing
+ * a pending plan).  coded_rows: multicast rows (the coded rate of eq. r2 for
+ * this draw); terms: rows the workers lack (the uncoded rate of eq. r1).
+ * Messages are ordered by group (bit mask, increasing), a group's rows by
+ * position j, and a message row's terms by worker. */
+coded_status coded_shuffle_plan(coded_shuffle* sh, int64_t* coded_rows, int64_t* terms);
+
+/* The pending plan's tables (host; any may be NULL):
+ *   enc_off      int64[coded_rows + 1]: message m's terms are [enc_off[m], enc_off[m+1])
+ *   enc_rows     int32[terms]: the data row of each term
+ *   term_worker  int32[terms]: the worker that lacks it
+ *   term_msg     int32[terms]: the message it belongs to
+ *   next_assign  int32[q]: the partition of iteration t+1 */
+coded_status coded_shuffle_tables(const coded_shuffle* sh, int64_t* enc_off, int32_t* enc_rows, int32_t* term_worker,
+                                  int32_t* term_msg, int32_t* next_assign);
+
+/* Applies the cache update rule for the pending plan and advances to t+1. */
+coded_status coded_shuffle_commit(coded_shuffle* sh);
+
+/* Device: M (coded_rows x r, row stride ldm) = the multicast rows, message m
+ * being the fp32 sum of the rows of its terms in order.  A is q x r fp32,
+ * row stride lda; the tables are device copies of coded_shuffle_tables'.  A
+ * message with a table entry out of range is written as NaN. */
+coded_status coded_shuffle_encode(const float* A, int64_t q, int64_t r, int64_t lda, const int64_t* enc_off,
+                                  const int32_t* enc_rows, int64_t coded_rows, int64_t terms, float* M, int64_t ldm,
+                                  void* stream);
+
+/* Device: out (terms x r, row stride ldo): row d is worker term_worker[d]'s
+ * copy of data row enc_rows[d], decoded as message term_msg[d] minus the
+ * other terms' rows of that message, in order (fp32).  A row whose table
+ * entries are out of range is written as NaN. */
+coded_status coded_shuffle_decode(const float* A, int64_t q, int64_t r, int64_t lda, const float* M, int64_t ldm,
+                                  const int64_t* enc_off, const int32_t* enc_rows, const int32_t* term_msg,
+                                  int64_t coded_rows, int64_t terms, float* out, int64_t ldo, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -43,6 +43,15 @@ _SIGNATURES = {
                                         _c_u64, _c_u64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_p, _c_i32, _c_p, _c_p,
                                         _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "coded_transpose": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i64, _c_p]),
+    "coded_shuffle_create": (_c_i32, [_c_i32, _c_i64, _c_i64, _c_u64, _c_p]),
+    "coded_shuffle_destroy": (_c_i32, [_c_p]),
+    "coded_shuffle_state": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
+    "coded_shuffle_plan": (_c_i32, [_c_p, _c_p, _c_p]),
+    "coded_shuffle_tables": (_c_i32, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "coded_shuffle_commit": (_c_i32, [_c_p]),
+    "coded_shuffle_encode": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_p, _c_i64, _c_p]),
+    "coded_shuffle_decode": (_c_i32, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_p, _c_i64, _c_i64,
+                                      _c_p, _c_i64, _c_p]),
     "coded_gd_sizes": (_c_i32, [_c_p, _c_p, _c_i64, _c_i64, _c_p]),
     "coded_gd_step": (_c_i32, [_c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_i64, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_dbl,
                                _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_p]),
@@ -357,3 +366,73 @@ def alloc_parity(code: Code, q: int, r: int, dtype, device="cuda"):
 def alloc_y(code: Code, q: int, s: int, dtype, device="cuda"):
     torch = _torch()
     return torch.empty((code.n, code.qb(q), s), dtype=dtype, device=device)
+
+
+class Shuffle:
+    """Coded-shuffling master state (coded_shuffle_create): n workers, q rows, caches of cache_rows rows."""
+
+    def __init__(self, n: int, q: int, cache_rows: int, seed: int):
+        h = ctypes.c_void_p()
+        _check(lib().coded_shuffle_create(n, q, cache_rows, seed, ctypes.byref(h)))
+        self.handle = h
+        self.n, self.q, self.cache_rows, self.seed = n, q, cache_rows, seed
+
+    def state(self):
+        """(t, partition int32[q], cache signatures uint64[q])."""
+        t = ctypes.c_int64()
+        assign = np.zeros(self.q, dtype=np.int32)
+        sig = np.zeros(self.q, dtype=np.uint64)
+        _check(lib().coded_shuffle_state(self.handle, ctypes.byref(t), assign.ctypes.data_as(ctypes.c_void_p),
+                                         sig.ctypes.data_as(ctypes.c_void_p)))
+        return t.value, assign, sig
+
+    def plan(self):
+        """Plans iteration t+1: (coded_rows, terms)."""
+        m, t = ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().coded_shuffle_plan(self.handle, ctypes.byref(m), ctypes.byref(t)))
+        self.coded_rows, self.terms = m.value, t.value
+        return m.value, t.value
+
+    def tables(self):
+        """The pending plan: dict of enc_off, enc_rows, term_worker, term_msg, next_assign (host arrays)."""
+        out = {"enc_off": np.zeros(self.coded_rows + 1, dtype=np.int64),
+               "enc_rows": np.zeros(self.terms, dtype=np.int32),
+               "term_worker": np.zeros(self.terms, dtype=np.int32),
+               "term_msg": np.zeros(self.terms, dtype=np.int32),
+               "next_assign": np.zeros(self.q, dtype=np.int32)}
+        _check(lib().coded_shuffle_tables(self.handle, *(out[k].ctypes.data_as(ctypes.c_void_p) for k in
+                                                         ("enc_off", "enc_rows", "term_worker", "term_msg",
+                                                          "next_assign"))))
+        return out
+
+    def commit(self):
+        _check(lib().coded_shuffle_commit(self.handle))
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().coded_shuffle_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def coded_shuffle_encode(A, enc_off, enc_rows, M, stream=None) -> None:
+    """M (coded_rows x r) from A (q x r fp32) and device copies of the plan's tables."""
+    q, r, lda = _matrix(A, "A")
+    coded_rows, _, ldm = _matrix(M, "M")
+    _check(lib().coded_shuffle_encode(_ptr(A), q, r, lda, _ptr(enc_off), _ptr(enc_rows), coded_rows,
+                                      enc_rows.numel(), _ptr(M), ldm, _stream(stream)))
+
+
+def coded_shuffle_decode(A, M, enc_off, enc_rows, term_msg, out, stream=None) -> None:
+    """out (terms x r): each worker's decoded copy of the rows it lacked."""
+    q, r, lda = _matrix(A, "A")
+    coded_rows, _, ldm = _matrix(M, "M")
+    _, _, ldo = _matrix(out, "out")
+    _check(lib().coded_shuffle_decode(_ptr(A), q, r, lda, _ptr(M), ldm, _ptr(enc_off), _ptr(enc_rows), _ptr(term_msg),
+                                      coded_rows, enc_rows.numel(), _ptr(out), ldo, _stream(stream)))
+

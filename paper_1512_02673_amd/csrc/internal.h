@@ -93,6 +93,14 @@ hipError_t launch_decode(const DecodeArgs& a, const DecodeSet* single, int mmax,
 hipError_t launch_transpose_f32(const float* A, int64_t q, int64_t r, int64_t lda, float* AT, int64_t ldat,
                                 hipStream_t st);
 
+// ---------------------------------------------------------------- coded shuffling
+hipError_t launch_shuffle_encode(const float* A, int64_t q, int64_t r, int64_t lda, const int64_t* off,
+                                 const int32_t* rows, int64_t msgs, int64_t terms, float* M, int64_t ldm,
+                                 hipStream_t st);
+hipError_t launch_shuffle_decode(const float* A, int64_t q, int64_t r, int64_t lda, const float* M, int64_t ldm,
+                                 const int64_t* off, const int32_t* rows, const int32_t* msg, int64_t msgs,
+                                 int64_t terms, float* out, int64_t ldo, hipStream_t st);
+
 // ---------------------------------------------------------------- runtime model
 hipError_t launch_runtime_sim(int n, int k, uint64_t seed, uint64_t first, int64_t count, double shift, double rate,
                               double* t_uncoded, double* t_repetition, double* t_mds, hipStream_t st);

@@ -1,0 +1,152 @@
+// Coded shuffling on the device (Sec. IV, Algorithm 1 and the decoding rule).
+//
+// encode: message row m is the sum of the data rows of its terms,
+//         enc_rows[enc_off[m] .. enc_off[m+1]), in that order;
+// decode: term d (row enc_rows[d], needed by one worker) is its message
+//         term_msg[d] minus the other terms' rows of that message, in order.
+// The data are coded over their own representation (fp32 sums and
+// differences, no fused operations), so a decoded row is bit-identical to a
+// sequential evaluation of the same sums.
+//
+// Both are row gathers bound by HBM: one wave per output row, 16-byte loads
+// when the rows allow them; a row's term loads are issued four at a time.
+// Every table entry is checked against its range: an entry outside it turns
+// its output row into NaN instead of reading out of bounds.
+#include "internal.h"
+
+namespace coded {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+typedef float f32x4s __attribute__((ext_vector_type(4)));
+
+template <int V>
+struct Row;
+template <>
+struct Row<4> {
+    typedef f32x4s T;
+    __device__ static T load(const float* p) { return *reinterpret_cast<const f32x4s*>(p); }
+    __device__ static void store(float* p, T v) { __builtin_nontemporal_store(v, reinterpret_cast<f32x4s*>(p)); }
+    __device__ static T nan() {
+        const float x = __builtin_nanf("");
+        return T{x, x, x, x};
+    }
+};
+template <>
+struct Row<1> {
+    typedef float T;
+    __device__ static T load(const float* p) { return *p; }
+    __device__ static void store(float* p, T v) { __builtin_nontemporal_store(v, p); }
+    __device__ static T nan() { return __builtin_nanf(""); }
+};
+
+// Validated term range of message m (false: a bad table entry).
+__device__ inline bool term_range(const int64_t* off, int64_t m, int64_t terms, int64_t& b, int64_t& e) {
+    b = off[m];
+    e = off[m + 1];
+    return 0 <= b && b <= e && e <= terms;
+}
+
+template <int V>
+__global__ __launch_bounds__(kThreads) void shuffle_encode_kernel(const float* __restrict__ A, int64_t q, int64_t r,
+                                                                  int64_t lda, const int64_t* __restrict__ off,
+                                                                  const int32_t* __restrict__ rows, int64_t msgs,
+                                                                  int64_t terms, float* __restrict__ M, int64_t ldm) {
+    using R = Row<V>;
+    const int lane = threadIdx.x & 63;
+    const int64_t m = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+    if (m >= msgs) return;
+    int64_t b, e;
+    bool ok = term_range(off, m, terms, b, e) && e > b;
+    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q;
+    float* dst = M + m * ldm;
+    for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
+        if (!ok) {
+            R::store(dst + c, R::nan());
+            continue;
+        }
+        typename R::T acc = R::load(A + static_cast<int64_t>(rows[b]) * lda + c);
+        int64_t t = b + 1;
+        for (; t + 4 <= e; t += 4) {
+            const typename R::T x0 = R::load(A + static_cast<int64_t>(rows[t]) * lda + c);
+            const typename R::T x1 = R::load(A + static_cast<int64_t>(rows[t + 1]) * lda + c);
+            const typename R::T x2 = R::load(A + static_cast<int64_t>(rows[t + 2]) * lda + c);
+            const typename R::T x3 = R::load(A + static_cast<int64_t>(rows[t + 3]) * lda + c);
+            acc = acc + x0;
+            acc = acc + x1;
+            acc = acc + x2;
+            acc = acc + x3;
+        }
+        for (; t < e; ++t) acc = acc + R::load(A + static_cast<int64_t>(rows[t]) * lda + c);
+        R::store(dst + c, acc);
+    }
+}
+
+template <int V>
+__global__ __launch_bounds__(kThreads) void shuffle_decode_kernel(const float* __restrict__ A, int64_t q, int64_t r,
+                                                                  int64_t lda, const float* __restrict__ M,
+                                                                  int64_t ldm, const int64_t* __restrict__ off,
+                                                                  const int32_t* __restrict__ rows,
+                                                                  const int32_t* __restrict__ msg, int64_t msgs,
+                                                                  int64_t terms, float* __restrict__ out,
+                                                                  int64_t ldo) {
+    using R = Row<V>;
+    const int lane = threadIdx.x & 63;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+    if (d >= terms) return;
+    const int64_t m = msg[d];
+    int64_t b = 0, e = 0;
+    bool ok = m >= 0 && m < msgs && term_range(off, m, terms, b, e) && b <= d && d < e;
+    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q;
+    float* dst = out + d * ldo;
+    for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
+        if (!ok) {
+            R::store(dst + c, R::nan());
+            continue;
+        }
+        typename R::T acc = R::load(M + m * ldm + c);
+        for (int64_t t = b; t < e; ++t)
+            if (t != d) acc = acc - R::load(A + static_cast<int64_t>(rows[t]) * lda + c);
+        R::store(dst + c, acc);
+    }
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) % 16) == 0; }
+
+}  // namespace
+
+hipError_t launch_shuffle_encode(const float* A, int64_t q, int64_t r, int64_t lda, const int64_t* off,
+                                 const int32_t* rows, int64_t msgs, int64_t terms, float* M, int64_t ldm,
+                                 hipStream_t st) {
+    if (msgs == 0 || r == 0) return hipSuccess;
+    const int64_t blocks = ceil_div(msgs, kWaves);
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const bool vec = r % 4 == 0 && lda % 4 == 0 && ldm % 4 == 0 && aligned16(A) && aligned16(M);
+    if (vec)
+        hipLaunchKernelGGL(shuffle_encode_kernel<4>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, st, A, q,
+                           r, lda, off, rows, msgs, terms, M, ldm);
+    else
+        hipLaunchKernelGGL(shuffle_encode_kernel<1>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, st, A, q,
+                           r, lda, off, rows, msgs, terms, M, ldm);
+    return hipGetLastError();
+}
+
+hipError_t launch_shuffle_decode(const float* A, int64_t q, int64_t r, int64_t lda, const float* M, int64_t ldm,
+                                 const int64_t* off, const int32_t* rows, const int32_t* msg, int64_t msgs,
+                                 int64_t terms, float* out, int64_t ldo, hipStream_t st) {
+    if (terms == 0 || r == 0) return hipSuccess;
+    const int64_t blocks = ceil_div(terms, kWaves);
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const bool vec = r % 4 == 0 && lda % 4 == 0 && ldm % 4 == 0 && ldo % 4 == 0 && aligned16(A) && aligned16(M) &&
+                     aligned16(out);
+    if (vec)
+        hipLaunchKernelGGL(shuffle_decode_kernel<4>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, st, A, q,
+                           r, lda, M, ldm, off, rows, msg, msgs, terms, out, ldo);
+    else
+        hipLaunchKernelGGL(shuffle_decode_kernel<1>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, st, A, q,
+                           r, lda, M, ldm, off, rows, msg, msgs, terms, out, ldo);
+    return hipGetLastError();
+}
+
+}  // namespace coded

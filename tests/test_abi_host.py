@@ -85,3 +85,41 @@ def test_optimal_k_matches_oracle(lib, n, mu):
     ks_ref, ts_ref, _ = rt.optimal_mds(n, mu)
     assert ks == pytest.approx(ks_ref, rel=1e-12) and ts == pytest.approx(ts_ref, rel=1e-12)
     assert kb == rt.best_integer_k(n, mu)
+
+
+@pytest.mark.parametrize("n,q,cache,seed", [(2, 4, 2, 0), (5, 200, 70, 3), (8, 4000, 1000, 11), (3, 18, 6, 1),
+                                            (16, 1600, 100, 7), (64, 640, 64, 2)])
+def test_shuffle_planner_matches_oracle_bit_exact(lib, n, q, cache, seed):
+    """The library's host planner (partition, caches, messages, cache rule) against
+    the oracle's, over three iterations."""
+    from oracle import shuffle as sh
+    st = lib.Shuffle(n, q, cache, seed)
+    ref = sh.initial_state(n, q, cache, seed)
+    for _ in range(3):
+        t, assign, sig = st.state()
+        assert t == ref.t
+        assert np.array_equal(assign, ref.assign)
+        assert np.array_equal(sig, sh.signatures(ref.cached))
+        coded_rows, terms = st.plan()
+        p = sh.plan(ref)
+        assert (coded_rows, terms) == (p.coded_rows, p.uncoded_rows)
+        tb = st.tables()
+        assert np.array_equal(tb["next_assign"], p.new_assign)
+        for key in ("enc_off", "enc_rows", "term_worker", "term_msg"):
+            assert np.array_equal(tb[key], getattr(p, key)), key
+        st.commit()
+        ref = sh.commit(ref, p)
+
+
+def test_shuffle_argument_errors(lib):
+    h = lib.lib()
+    out = ctypes.c_void_p()
+    assert h.coded_shuffle_create(0, 10, 5, 0, ctypes.byref(out)) == lib.CODED_ERR_ARG
+    assert h.coded_shuffle_create(65, 650, 50, 0, ctypes.byref(out)) == lib.CODED_ERR_ARG
+    assert h.coded_shuffle_create(3, 10, 5, 0, ctypes.byref(out)) == lib.CODED_ERR_SHAPE      # 3 does not divide 10
+    assert h.coded_shuffle_create(2, 10, 4, 0, ctypes.byref(out)) == lib.CODED_ERR_ARG        # cache < q/n
+    st = lib.Shuffle(2, 10, 6, 0)
+    with pytest.raises(lib.CodedError):
+        st.commit()                                          # nothing planned
+    assert h.coded_shuffle_tables(st.handle, None, None, None, None, None) == lib.CODED_ERR_ARG
+    assert h.coded_shuffle_plan(None, None, None) == lib.CODED_ERR_ARG
