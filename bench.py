@@ -644,6 +644,98 @@ def straggler_workload(args):
     }
 
 
+def shuffle_workload(args):
+    """Coded shuffling (Sec. IV) with the paper's cache fraction s/q = 0.1
+    and n = 16 workers, q = 10^6 rows of 256 fp32 (1 GB): a regime where the
+    law-of-large-numbers step of Theorem 1 holds (the number of worker groups
+    a row can fall into stays far below q).  One step is one iteration: the host plans Algorithm 1 for a fresh
+    random partition, the device encodes the multicast rows and decodes every
+    worker's missing rows, and the host applies the cache rule.  Unit: decoded
+    rows per second of device time (encode + decode); the host planning time
+    and the communication rates (measured vs eqs. r1 and r2) are reported
+    beside it."""
+    import torch
+
+    from paper_1512_02673_amd import binding as lib
+
+    n, q, r, cache, seed = 16, 1_000_000, 256, 100_000, 8
+    K, W = args.steps, args.warmup
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    dA = torch.from_numpy(A).cuda()
+    st = lib.Shuffle(n, q, cache, seed)
+    stream = torch.cuda.current_stream()
+    rec = []
+    for it in range(W + K):
+        t0 = time.perf_counter()
+        coded_rows, terms = st.plan()
+        tb = st.tables()
+        t_plan = time.perf_counter() - t0
+        dev = {k: torch.from_numpy(tb[k]).cuda() for k in ("enc_off", "enc_rows", "term_msg")}
+        M = torch.empty((coded_rows, r), dtype=torch.float32, device="cuda")
+        out = torch.empty((terms, r), dtype=torch.float32, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        lib.coded_shuffle_encode(dA, dev["enc_off"], dev["enc_rows"], M)
+        ev[1].record(stream)
+        lib.coded_shuffle_decode(dA, M, dev["enc_off"], dev["enc_rows"], dev["term_msg"], out)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        st.commit()
+        t_commit = time.perf_counter() - t1
+        c = np.diff(tb["enc_off"]).astype(np.float64)            # terms per message row
+        enc_bytes = 4.0 * r * (terms + coded_rows)
+        dec_bytes = 4.0 * r * (float(np.sum(c * c)) + terms)       # message + other terms read, one row written
+        if it >= W:
+            rec.append((coded_rows, terms, t_plan, t_commit, ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]),
+                        enc_bytes, dec_bytes))
+        del M, out, dev
+    a = np.array(rec)
+    enc_ms, dec_ms = float(a[:, 4].mean()), float(a[:, 5].mean())
+    enc_gbs = float(np.mean(a[:, 6] / (a[:, 4] * 1e-3))) / 1e9
+    dec_gbs = float(np.mean(a[:, 7] / (a[:, 5] * 1e-3))) / 1e9
+    s_rows = cache
+
+    def harm_rate_coded():
+        pp = (s_rows - q / n) / (q - q / n)
+        return q / (n * pp) ** 2 * ((1 - pp) ** (n + 1) + (n - 1) * pp * (1 - pp) - (1 - pp) ** 2)
+    result = {
+        "metric": METRIC, "value": float(np.sum(a[:, 1]) / np.sum((a[:, 4] + a[:, 5]) * 1e-3)),
+        "unit": "decoded rows/s (device encode + decode)", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": float(np.mean((a[:, 4] + a[:, 5]))), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "shuffle16_1000000x256", "n": n, "q": q, "r": r, "cache_rows": cache, "seed": seed},
+        "rates_rows_per_iteration": {
+            "coded_measured": float(a[:, 0].mean()), "uncoded_measured": float(a[:, 1].mean()),
+            "coded_theorem_eq_r2": harm_rate_coded(), "uncoded_eq_r1": q * (1 - s_rows / q),
+            "reduction_measured": 1 - float(a[:, 0].mean() / a[:, 1].mean())},
+        "host_ms": {"plan": float(a[:, 2].mean()) * 1e3, "cache_rule": float(a[:, 3].mean()) * 1e3},
+        "encode_ms": enc_ms, "decode_ms": dec_ms,
+        "roofline": {"bound": "hbm", "kernel": "shuffle_decode_kernel", "achieved": dec_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": dec_gbs / HBM_PEAK_GBS,
+                     "algorithmic_bytes_per_launch": float(a[:, 7].mean()), "traffic": None,
+                     "encode_achieved_gbs": enc_gbs},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import shuffle as sh
+        # the oracle's encode and decode on the first messages of one plan of the same state
+        coded_rows, terms = st.plan()
+        tb = st.tables()
+        mcount = coded_rows                       # one whole iteration (a few seconds of CPU)
+        off = tb["enc_off"][:mcount + 1]
+        sub = sh.Plan(tb["next_assign"], [], off, tb["enc_rows"][:off[-1]], tb["term_worker"][:off[-1]],
+                      tb["term_msg"][:off[-1]], mcount, int(off[-1]))
+        t0 = time.perf_counter()
+        sh.decode(A, sh.encode(A, sub), sub)
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": sub.uncoded_rows / el, "unit": "decoded rows/s (encode + decode)",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"all {mcount} messages ({sub.uncoded_rows} decoded rows) of one "
+                                            f"iteration's plan, oracle encode + decode in {el:.1f} s"}
+    return result
+
+
 def calibrate_copy(nbytes: int, reps: int):
     """A plain device copy of known size, for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -664,7 +756,7 @@ def main():
                     choices=["gemv16x12_65536x8192", "gemv16x12_conditioned_65536x8192",
                              "decode64x48_16384x4096x8", "gd20x16_262144x4096",
                              "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
-                             "straggler16x12_65536x8192"])
+                             "straggler16x12_65536x8192", "shuffle16_1000000x256"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-products", type=int, default=300)
     ap.add_argument("--cpu-decodes", type=int, default=1000)
@@ -704,6 +796,12 @@ def main():
         if "--warmup" not in sys.argv:
             args.warmup = 2
         result = runtime_sim_workload(args)
+    elif args.workload == "shuffle16_1000000x256":
+        if "--steps" not in sys.argv:
+            args.steps = 5
+        if "--warmup" not in sys.argv:
+            args.warmup = 1
+        result = shuffle_workload(args)
     elif args.workload == "straggler16x12_65536x8192":
         if "--steps" not in sys.argv:
             args.steps = 100
