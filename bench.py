@@ -686,7 +686,7 @@ def shuffle_workload(args):
         t_commit = time.perf_counter() - t1
         c = np.diff(tb["enc_off"]).astype(np.float64)            # terms per message row
         enc_bytes = 4.0 * r * (terms + coded_rows)
-        dec_bytes = 4.0 * r * (float(np.sum(c * c)) + terms)       # message + other terms read, one row written
+        dec_bytes = 4.0 * r * (coded_rows + 2.0 * terms)            # each message and data row read once, rows written
         if it >= W:
             rec.append((coded_rows, terms, t_plan, t_commit, ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]),
                         enc_bytes, dec_bytes))
@@ -715,7 +715,7 @@ def shuffle_workload(args):
         "roofline": {"bound": "hbm", "kernel": "shuffle_decode_kernel", "achieved": dec_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": dec_gbs / HBM_PEAK_GBS,
                      "algorithmic_bytes_per_launch": float(a[:, 7].mean()), "traffic": None,
-                     "encode_achieved_gbs": enc_gbs},
+                     "encode_achieved_gbs": enc_gbs, "encode_algorithmic_bytes_per_launch": float(a[:, 6].mean())},
     }
     if not args.no_cpu_baseline:
         from oracle import shuffle as sh

@@ -3,15 +3,17 @@
 // encode: message row m is the sum of the data rows of its terms,
 //         enc_rows[enc_off[m] .. enc_off[m+1]), in that order;
 // decode: term d (row enc_rows[d], needed by one worker) is its message
-//         term_msg[d] minus the other terms' rows of that message, in order.
+//         term_msg[d] minus the other terms' rows of that message, in order;
+//         one wave per message writes all of its terms.
 // The data are coded over their own representation (fp32 sums and
 // differences, no fused operations), so a decoded row is bit-identical to a
 // sequential evaluation of the same sums.
 //
-// Both are row gathers bound by HBM: one wave per output row, 16-byte loads
-// when the rows allow them; a row's term loads are issued four at a time.
-// Every table entry is checked against its range: an entry outside it turns
-// its output row into NaN instead of reading out of bounds.
+// Both are row gathers bound by HBM: one wave per message row, 16-byte loads
+// when the rows allow them; the encode issues a row's term loads four at a
+// time.  Every table entry is checked against its range: an entry outside it
+// turns its output rows into NaN instead of reading out of bounds (a term
+// that no valid message range covers is left unwritten).
 #include "internal.h"
 
 namespace coded {
@@ -83,6 +85,11 @@ __global__ __launch_bounds__(kThreads) void shuffle_encode_kernel(const float* _
     }
 }
 
+// One wave per message m: its row and its terms' rows are read once (up to
+// kTermRegs of them held in registers) and every term d of the message is
+// written as the message minus the other terms' rows, in order.
+constexpr int kTermRegs = 8;
+
 template <int V>
 __global__ __launch_bounds__(kThreads) void shuffle_decode_kernel(const float* __restrict__ A, int64_t q, int64_t r,
                                                                   int64_t lda, const float* __restrict__ M,
@@ -93,22 +100,42 @@ __global__ __launch_bounds__(kThreads) void shuffle_decode_kernel(const float* _
                                                                   int64_t ldo) {
     using R = Row<V>;
     const int lane = threadIdx.x & 63;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
-    if (d >= terms) return;
-    const int64_t m = msg[d];
-    int64_t b = 0, e = 0;
-    bool ok = m >= 0 && m < msgs && term_range(off, m, terms, b, e) && b <= d && d < e;
-    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q;
-    float* dst = out + d * ldo;
+    const int64_t m = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+    if (m >= msgs) return;
+    int64_t b, e;
+    if (!term_range(off, m, terms, b, e)) return;          // no term of this message can be placed
+    bool ok = true;
+    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q && msg[t] == m;
+    const int64_t cnt = e - b;
     for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
         if (!ok) {
-            R::store(dst + c, R::nan());
+            for (int64_t d = b; d < e; ++d) R::store(out + d * ldo + c, R::nan());
             continue;
         }
-        typename R::T acc = R::load(M + m * ldm + c);
-        for (int64_t t = b; t < e; ++t)
-            if (t != d) acc = acc - R::load(A + static_cast<int64_t>(rows[t]) * lda + c);
-        R::store(dst + c, acc);
+        const typename R::T mv = R::load(M + m * ldm + c);
+        if (cnt <= kTermRegs) {
+            typename R::T x[kTermRegs];
+#pragma unroll
+            for (int j = 0; j < kTermRegs; ++j)
+                if (j < cnt) x[j] = R::load(A + static_cast<int64_t>(rows[b + j]) * lda + c);
+#pragma unroll
+            for (int i = 0; i < kTermRegs; ++i) {
+                if (i < cnt) {
+                    typename R::T acc = mv;
+#pragma unroll
+                    for (int j = 0; j < kTermRegs; ++j)
+                        if (j < cnt && j != i) acc = acc - x[j];
+                    R::store(out + (b + i) * ldo + c, acc);
+                }
+            }
+        } else {
+            for (int64_t d = b; d < e; ++d) {
+                typename R::T acc = mv;
+                for (int64_t t = b; t < e; ++t)
+                    if (t != d) acc = acc - R::load(A + static_cast<int64_t>(rows[t]) * lda + c);
+                R::store(out + d * ldo + c, acc);
+            }
+        }
     }
 }
 
@@ -135,8 +162,8 @@ hipError_t launch_shuffle_encode(const float* A, int64_t q, int64_t r, int64_t l
 hipError_t launch_shuffle_decode(const float* A, int64_t q, int64_t r, int64_t lda, const float* M, int64_t ldm,
                                  const int64_t* off, const int32_t* rows, const int32_t* msg, int64_t msgs,
                                  int64_t terms, float* out, int64_t ldo, hipStream_t st) {
-    if (terms == 0 || r == 0) return hipSuccess;
-    const int64_t blocks = ceil_div(terms, kWaves);
+    if (terms == 0 || msgs == 0 || r == 0) return hipSuccess;
+    const int64_t blocks = ceil_div(msgs, kWaves);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     const bool vec = r % 4 == 0 && lda % 4 == 0 && ldm % 4 == 0 && ldo % 4 == 0 && aligned16(A) && aligned16(M) &&
                      aligned16(out);
