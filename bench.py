@@ -36,9 +36,18 @@ KERNEL_SOURCES = ["paper_1512_02673_amd/csrc/worker.hip", "paper_1512_02673_amd/
                   "paper_1512_02673_amd/csrc/internal.h"]
 
 
-def kernel_source_hash() -> str:
+# Runtime-model kernel: executed VALU instructions per launch from a committed
+# rocprofv3 counter summary (SQ_INSTS_VALU), valid for this source hash only.
+VALU_FILE = os.path.join(ROOT, "profiles", "runtime_sim_valu_10x5.json")
+RUNTIME_SOURCES = ["paper_1512_02673_amd/csrc/runtime.hip", "paper_1512_02673_amd/csrc/internal.h"]
+# Vector-issue peak: 256 CUs x 4 SIMDs, one wave64 VALU instruction per SIMD
+# every 4 cycles (16 lanes wide) at 2.4 GHz = 614.4 G wave-instructions/s.
+ALU_PEAK_G = 256 * 4 * 2.4 / 4
+
+
+def kernel_source_hash(sources=None) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in sources or KERNEL_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -57,6 +66,19 @@ def measured_traffic(per_launch_algorithmic: float):
     if abs(float(t.get("algorithmic_bytes_per_launch", -1.0)) - per_launch_algorithmic) > 1.0:
         return None                      # counters of another launch shape
     return float(t["hbm_bytes_per_launch"])
+
+
+def measured_valu(draws: int):
+    """Executed VALU wave-instructions per runtime-model launch of `draws`
+    draws, or None when the summary is missing or for another source."""
+    try:
+        with open(VALU_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash(RUNTIME_SOURCES) or t.get("draws_per_launch") != draws:
+        return None
+    return float(t["valu_insts_per_launch"])
 
 
 def blas_threads() -> int:
@@ -542,7 +564,8 @@ def runtime_sim_workload(args):
     elapsed = time.perf_counter() - start
     ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     means = [float(t.mean().item()) for t in out]
-    wbytes = 24.0 * draws
+    valu = measured_valu(draws)
+    achieved = valu / (ms * 1e-3) / 1e9 if valu is not None else None
     result = {
         "metric": METRIC, "value": K * draws / elapsed, "unit": "simulated draws/s", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak",
@@ -550,22 +573,25 @@ def runtime_sim_workload(args):
         "config": {"workload": "runtime_sim_10x5", "n": n, "k": k, "shift": 1.0, "rate": 1.0,
                    "draws_per_step": draws, "schemes": ["uncoded", "repetition", "mds"]},
         "means_last_step": dict(zip(["uncoded", "repetition", "mds"], means)),
-        "roofline": {"bound": "alu", "kernel": "runtime_sim_kernel",
-                     "note": "integer-ALU bound: 64-bit SplitMix64 words and O(n^2) ranking per draw; "
-                             "the output writes use only the fraction of HBM given here",
-                     "achieved": wbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": wbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                     "algorithmic_bytes_per_launch": wbytes, "traffic": None},
+        "roofline": {"bound": "alu", "kernel": "runtime_sim_kernel<12>",
+                     "note": "vector-issue bound: 64-bit SplitMix64 words and the O(n^2) ranking per draw; "
+                             "achieved = executed VALU wave-instructions per launch (SQ_INSTS_VALU) / launch time",
+                     "achieved": achieved, "peak": ALU_PEAK_G, "unit": "G wave-instructions/s",
+                     "frac": achieved / ALU_PEAK_G if achieved is not None else None,
+                     "valu_insts_per_launch": valu, "hbm_write_gbs": 24.0 * draws / (ms * 1e-3) / 1e9,
+                     "traffic": None},
     }
     if not args.no_cpu_baseline:
         from oracle import runtime as rt
-        cnt = 1 << 21
+        chunk, chunks = 1 << 21, 16
         t0 = time.perf_counter()
-        rt.simulate(n, k, seed, 0, cnt)
+        for c in range(chunks):
+            rt.simulate(n, k, seed, c * chunk, chunk)
         el = time.perf_counter() - t0
+        cnt = chunk * chunks
         result["cpu_baseline"] = {"value": cnt / el, "unit": "simulated draws/s", "cores": blas_threads(),
                                   "kind": "oracle", "sample": f"{cnt} draws of the same simulation with the NumPy "
-                                                              f"oracle in {el:.1f} s"}
+                                                              f"oracle, {chunks} calls of {chunk}, in {el:.1f} s"}
     return result
 
 

@@ -8,7 +8,8 @@
 //   MDS (n,k)    subtasks of T0/k, the k-th finisher (eq. mds_coded).
 // T0 falls as the word grows, so every order statistic is taken on the
 // integer words and only the selected word goes through the logarithm.
-// One thread per draw; words live in registers for n <= 64 and are
+// One thread per draw; words live in registers for n <= 32 (loops unrolled
+// over the register count, so no word is indexed at run time) and are
 // recomputed for larger n.
 #include "internal.h"
 
@@ -18,11 +19,21 @@ namespace {
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kRuntimeStream = 4;
 
-__device__ inline uint64_t word_of(uint64_t seed, uint64_t draw, uint64_t worker) {
-    uint64_t z = seed + (((kRuntimeStream << 56) | (draw << 16) | worker) + 1) * kGamma;
+// SplitMix64 output of counter c is mix(seed + (c + 1) * gamma).  With the
+// counter 4 << 56 | draw << 16 | worker (worker < 2^16, so the OR is a sum)
+// the state is base(draw) + worker * gamma, modulo 2^64.
+__device__ inline uint64_t mix(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
     z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
     return z ^ (z >> 31);
+}
+
+__device__ inline uint64_t base_of(uint64_t seed, uint64_t draw) {
+    return seed + (((kRuntimeStream << 56) | (draw << 16)) + 1) * kGamma;
+}
+
+__device__ inline uint64_t word_of(uint64_t base, int worker) {
+    return mix(base + static_cast<uint64_t>(worker) * kGamma);
 }
 
 __device__ inline double mother(uint64_t w, double shift, double rate) {
@@ -39,51 +50,96 @@ __global__ __launch_bounds__(256) void runtime_sim_kernel(int n, int k, uint64_t
                                                           double* t_mds) {
     const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (d >= count) return;
-    const uint64_t draw = first_draw + static_cast<uint64_t>(d);
-    uint64_t u[NMAX > 0 ? NMAX : 1];
-    auto W = [&](int i) -> uint64_t {
-        if constexpr (NMAX > 0) return u[i];
-        else return word_of(seed, draw, static_cast<uint64_t>(i));
-    };
+    const uint64_t base = base_of(seed, first_draw + static_cast<uint64_t>(d));
     if constexpr (NMAX > 0) {
+        // Words in registers: every loop runs over the compile-time NMAX with
+        // uniform guards (i < n), so each register index is a constant.
+        uint64_t u[NMAX];
 #pragma unroll
-        for (int i = 0; i < NMAX; ++i)
-            if (i < n) u[i] = word_of(seed, draw, static_cast<uint64_t>(i));
-    }
-    // uncoded: the slowest worker = the smallest word (ties: the higher index finishes later)
-    if (t_unc) {
-        int slow = 0;
-        uint64_t us = W(0);
-        for (int i = 1; i < n; ++i) {
-            const uint64_t ui = W(i);
-            if (before(us, slow, ui, i)) { us = ui; slow = i; }
+        for (int i = 0; i < NMAX; ++i) u[i] = i < n ? word_of(base, i) : 0;
+        if (t_unc) {
+            // the slowest worker: the smallest word (ties: the higher index finishes later)
+            int slow = 0;
+            uint64_t us = u[0];
+#pragma unroll
+            for (int i = 1; i < NMAX; ++i)
+                if (i < n && before(us, slow, u[i], i)) {
+                    us = u[i];
+                    slow = i;
+                }
+            t_unc[d] = mother(us, shift, rate) / n;
         }
-        t_unc[d] = mother(us, shift, rate) / n;
-    }
-    // MDS: the k-th finisher is the worker with exactly k-1 workers before it
-    if (t_mds) {
-        uint64_t uk = 0;
-        for (int i = 0; i < n; ++i) {
-            const uint64_t ui = W(i);
-            int rank = 0;
-            for (int j = 0; j < n; ++j) rank += j != i && before(W(j), j, ui, i);
-            if (rank == k - 1) uk = ui;
-        }
-        t_mds[d] = mother(uk, shift, rate) / k;
-    }
-    // repetition: per task the fastest replica (largest word), then the slowest task
-    if (t_rep) {
-        const int g = n / k;
-        uint64_t worst = ~0ull;
-        for (int task = 0; task < k; ++task) {
-            uint64_t best = 0;
-            for (int j = 0; j < g; ++j) {
-                const uint64_t uj = W(task * g + j);
-                best = uj > best ? uj : best;
+        if (t_mds) {
+            // the k-th finisher: the worker with exactly k-1 workers before it
+            uint64_t uk = 0;
+#pragma unroll
+            for (int i = 0; i < NMAX; ++i) {
+                if (i < n) {
+                    int rank = 0;
+#pragma unroll
+                    for (int j = 0; j < NMAX; ++j)
+                        if (j < n && j != i) rank += before(u[j], j, u[i], i) ? 1 : 0;
+                    uk = rank == k - 1 ? u[i] : uk;
+                }
             }
-            worst = best < worst ? best : worst;
+            t_mds[d] = mother(uk, shift, rate) / k;
         }
-        t_rep[d] = mother(worst, shift, rate) / k;
+        if (t_rep) {
+            // per task (n/k consecutive workers) the fastest replica, then the slowest task
+            const int g = n / k;
+            uint64_t worst = ~0ull, best = 0;
+            int pos = 0;
+#pragma unroll
+            for (int i = 0; i < NMAX; ++i) {
+                if (i < n) {
+                    best = u[i] > best ? u[i] : best;
+                    if (++pos == g) {
+                        worst = best < worst ? best : worst;
+                        best = 0;
+                        pos = 0;
+                    }
+                }
+            }
+            t_rep[d] = mother(worst, shift, rate) / k;
+        }
+    } else {
+        // n > 32: words recomputed where needed
+        auto W = [&](int i) { return word_of(base, i); };
+        if (t_unc) {
+            int slow = 0;
+            uint64_t us = W(0);
+            for (int i = 1; i < n; ++i) {
+                const uint64_t ui = W(i);
+                if (before(us, slow, ui, i)) {
+                    us = ui;
+                    slow = i;
+                }
+            }
+            t_unc[d] = mother(us, shift, rate) / n;
+        }
+        if (t_mds) {
+            uint64_t uk = 0;
+            for (int i = 0; i < n; ++i) {
+                const uint64_t ui = W(i);
+                int rank = 0;
+                for (int j = 0; j < n; ++j) rank += j != i && before(W(j), j, ui, i);
+                if (rank == k - 1) uk = ui;
+            }
+            t_mds[d] = mother(uk, shift, rate) / k;
+        }
+        if (t_rep) {
+            const int g = n / k;
+            uint64_t worst = ~0ull;
+            for (int task = 0; task < k; ++task) {
+                uint64_t best = 0;
+                for (int j = 0; j < g; ++j) {
+                    const uint64_t uj = W(task * g + j);
+                    best = uj > best ? uj : best;
+                }
+                worst = best < worst ? best : worst;
+            }
+            t_rep[d] = mother(worst, shift, rate) / k;
+        }
     }
 }
 
@@ -102,9 +158,11 @@ hipError_t launch_sim(int n, int k, uint64_t seed, uint64_t first, int64_t count
 hipError_t launch_runtime_sim(int n, int k, uint64_t seed, uint64_t first, int64_t count, double shift, double rate,
                               double* tu, double* tr, double* tm, hipStream_t st) {
     if (count == 0) return hipSuccess;
+    if (n <= 8) return launch_sim<8>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
+    if (n <= 12) return launch_sim<12>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
     if (n <= 16) return launch_sim<16>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
+    if (n <= 24) return launch_sim<24>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
     if (n <= 32) return launch_sim<32>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
-    if (n <= 64) return launch_sim<64>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
     return launch_sim<0>(n, k, seed, first, count, shift, rate, tu, tr, tm, st);
 }
 
