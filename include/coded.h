@@ -115,7 +115,11 @@ coded_status coded_sizes(const coded_code* code, coded_dtype dt, coded_dtype y_d
  * systematic blocks are A itself and are not copied).  Rows of A at or beyond
  * q are the zero padding of Sec. III-A's footnote and are never read.
  *   dt        CODED_F32: sums in fp64; CODED_BF16: every P entry must be a
- *             bfloat16 value (else CODED_ERR_ARG), sums in fp32.
+ *             bfloat16 value (else CODED_ERR_ARG), sums in fp32.  For bf16
+ *             codes with k = 24, n - k = 8 and two planes, r a multiple of 64,
+ *             lda a multiple of 8 and A, parity 16-byte aligned, each column's
+ *             sum is formed on the matrix cores (exact products, one fp32
+ *             result); coded_encode_worker_mm writes the same planes.
  *   A         device, q x r of dt, row stride lda.
  *   parity    device, the parity buffer (layout above), written in full.
  */
@@ -141,6 +145,24 @@ coded_status coded_encode(const coded_code* code, coded_dtype dt, const void* A,
 coded_status coded_worker_mm(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                              const void* parity, const void* X, int64_t s, int64_t ldx, const uint8_t* worker_mask,
                              void* Y, coded_dtype y_dt, void* workspace, void* stream);
+
+/*
+ * coded_encode_worker_mm -- the parity blocks and all n worker products in
+ * one call (Sec. III-A: the master encodes the sub-matrices, every worker
+ * multiplies its block by the multicast input).  The result equals
+ * coded_encode followed by coded_worker_mm for every worker: parity is written
+ * exactly as coded_encode writes it, and Y holds every worker's product.  For
+ * the bf16 shapes coded_encode forms on the matrix cores, with s = 64 and a
+ * 16-byte aligned workspace, A is read from memory once for both (the parity
+ * rows feed the products from on-chip memory); other inputs run the two steps
+ * one after the other.  Products of one worker may be summed in another order
+ * than coded_worker_mm's (fp32 accumulation; equal within rounding).
+ *   A, X, s, ldx, Y, y_dt, workspace as for coded_worker_mm (workspace is
+ *   required for bf16 inputs); parity as for coded_encode.
+ */
+coded_status coded_encode_worker_mm(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r,
+                                    int64_t lda, void* parity, const void* X, int64_t s, int64_t ldx, void* Y,
+                                    coded_dtype y_dt, void* workspace, void* stream);
 
 /*
  * coded_decode -- dec(indices, results) of Sec. III-A for one survivor set.

@@ -32,6 +32,8 @@ _SIGNATURES = {
     "coded_encode": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p]),
     "coded_worker_mm": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64, _c_p,
                                  _c_p, _c_i32, _c_p, _c_p]),
+    "coded_encode_worker_mm": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64,
+                                        _c_p, _c_i32, _c_p, _c_p]),
     "coded_decode": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p]),
     "coded_decode_batched": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_i32, _c_i64, _c_i64, _c_p, _c_i64, _c_i64,
                                       _c_p, _c_p]),
@@ -255,6 +257,19 @@ def coded_worker_mm(code: Code, A, parity, X, Y, worker_mask=None, workspace="au
         workspace = worker_workspace(code, A, X)
     _check(lib().coded_worker_mm(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _ptr(X), s, ldx,
                                  mask, _ptr(Y), _dtype_code(Y), _ptr(workspace), _stream(stream)))
+
+
+def coded_encode_worker_mm(code: Code, A, parity, X, Y, workspace="auto", stream=None) -> None:
+    """Parity blocks and every worker's product in one call (coded_encode, then
+    coded_worker_mm for all workers; one pass over A where the kernel serves the shape)."""
+    q, r, lda = _matrix(A, "A")
+    rx, s, ldx = _matrix(X, "X")
+    if rx != r:
+        raise ValueError("X must have r rows")
+    if isinstance(workspace, str):
+        workspace = worker_workspace(code, A, X)
+    _check(lib().coded_encode_worker_mm(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), _ptr(X), s,
+                                        ldx, _ptr(Y), _dtype_code(Y), _ptr(workspace), _stream(stream)))
 
 
 def coded_decode(code: Code, survivors, Y, q: int, out, info, stream=None) -> None:

@@ -94,6 +94,32 @@ bool is_bf16_value(double v) {
     return (b & 0xFFFFu) == 0;
 }
 
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// bf16 shapes served by the single-pass encode (and encode + products) kernel.
+bool single_pass_bf16(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                      const void* parity) {
+    return dt == CODED_BF16 && q > 0 && c->dPf && fused_bf16_supported(c->n, c->k, c->planes, r, lda) &&
+           aligned16(A) && aligned16(parity);
+}
+
+FusedArgs fused_args(const coded_code* c, const void* A, int64_t q, int64_t r, int64_t lda, void* parity,
+                     const void* xt, void* Y) {
+    FusedArgs f{};
+    f.A = static_cast<const uint16_t*>(A);
+    f.parity = static_cast<uint16_t*>(parity);
+    f.xt = static_cast<const uint16_t*>(xt);
+    f.Y = static_cast<float*>(Y);
+    f.P = c->dPf;
+    f.q = q;
+    f.r = r;
+    f.lda = lda;
+    f.qb = block_rows(q, c->k);
+    f.n = c->n;
+    f.k = c->k;
+    return f;
+}
+
 coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                        void* parity, hipStream_t st) {
     const int64_t qb = block_rows(q, c->k);
@@ -105,8 +131,13 @@ coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64
             if (!is_bf16_value(c->G[i]))
                 return fail(CODED_ERR_ARG, "bf16 encode needs every parity coefficient to be a bfloat16 value");
     }
-    EncodeArgs a{A, parity, c->dG, q, r, lda, qb, c->n, c->k, c->planes};
-    hipError_t e = dt == CODED_F32 ? launch_encode_f32(a, st) : launch_encode_bf16(a, st);
+    hipError_t e;
+    if (single_pass_bf16(c, dt, A, q, r, lda, parity)) {
+        e = launch_fused_bf16(fused_args(c, A, q, r, lda, parity, nullptr, nullptr), false, c->compute_units, st);
+    } else {
+        EncodeArgs a{A, parity, c->dG, q, r, lda, qb, c->n, c->k, c->planes};
+        e = dt == CODED_F32 ? launch_encode_f32(a, st) : launch_encode_bf16(a, st);
+    }
     if (e != hipSuccess) return hip_fail(e, "encode launch");
     return CODED_OK;
 }
@@ -154,6 +185,34 @@ coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int6
     }
     hipError_t e = dt == CODED_F32 ? launch_worker_f32(a, st) : launch_worker_bf16(a, st);
     if (e != hipSuccess) return hip_fail(e, "worker launch");
+    return CODED_OK;
+}
+
+// Parity blocks, then every worker's product.  bf16 inputs of a shape the
+// single-pass kernel serves, with 64 columns, read A once for both; any
+// other input runs the encode and the products one after the other.
+coded_status do_encode_workers(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
+                               void* parity, const void* X, int64_t s, int64_t ldx, void* Y, coded_dtype y_dt,
+                               void* workspace, hipStream_t st) {
+    const bool one_pass = single_pass_bf16(c, dt, A, q, r, lda, parity) && s == 64 && ldx >= 64 && X && Y &&
+                          workspace && aligned16(workspace) && y_dt == CODED_F32;
+    if (!one_pass) {
+        if (coded_status e = do_encode(c, dt, A, q, r, lda, parity, st)) return e;
+        return do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, Y, y_dt, workspace, st);
+    }
+    for (size_t i = static_cast<size_t>(c->k) * c->k; i < c->G.size(); ++i)
+        if (!is_bf16_value(c->G[i]))
+            return fail(CODED_ERR_ARG, "bf16 encode needs every parity coefficient to be a bfloat16 value");
+    WorkerArgs xa{};
+    xa.X = X;
+    xa.r = r;
+    xa.s = s;
+    xa.ldx = ldx;
+    xa.xt = workspace;
+    hipError_t e = launch_transpose_x_bf16(xa, st);
+    if (e == hipSuccess)
+        e = launch_fused_bf16(fused_args(c, A, q, r, lda, parity, workspace, Y), true, c->compute_units, st);
+    if (e != hipSuccess) return hip_fail(e, "encode and worker launch");
     return CODED_OK;
 }
 
@@ -224,7 +283,15 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
     hipError_t e = hipGetDevice(&c->device);
     if (e == hipSuccess) e = hipMalloc(&c->dG, c->G.size() * sizeof(double));
     if (e == hipSuccess) e = hipMemcpy(c->dG, c->G.data(), c->G.size() * sizeof(double), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&c->compute_units, hipDeviceAttributeMultiprocessorCount, c->device);
+    if (e == hipSuccess && n > k) {
+        std::vector<float> pf(static_cast<size_t>(n - k) * k);
+        for (size_t i = 0; i < pf.size(); ++i) pf[i] = static_cast<float>(c->G[static_cast<size_t>(k) * k + i]);
+        e = hipMalloc(&c->dPf, pf.size() * sizeof(float));
+        if (e == hipSuccess) e = hipMemcpy(c->dPf, pf.data(), pf.size() * sizeof(float), hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
+        if (c->dPf) (void)hipFree(c->dPf);
         if (c->dG) (void)hipFree(c->dG);
         delete c;
         return hip_fail(e, "coded_code_create");
@@ -242,6 +309,10 @@ coded_status coded_code_destroy(coded_code* c) {
     if (c->start_event) hipEventDestroy(c->start_event);
     for (hipStream_t w : c->worker_streams) hipStreamDestroy(w);
     if (c->dG) e = hipFree(c->dG);
+    if (c->dPf) {
+        const hipError_t e2 = hipFree(c->dPf);
+        if (e == hipSuccess) e = e2;
+    }
     delete c;
     if (e != hipSuccess) return hip_fail(e, "coded_code_destroy");
     return CODED_OK;
@@ -293,6 +364,23 @@ coded_status coded_worker_mm(const coded_code* c, coded_dtype dt, const void* A,
     if (coded_status st = check_ar(q, r, lda)) return st;
     return do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, worker_mask, Y, y_dt, workspace,
                       static_cast<hipStream_t>(stream));
+    CODED_GUARD_END
+}
+
+coded_status coded_encode_worker_mm(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r,
+                                    int64_t lda, void* parity, const void* X, int64_t s, int64_t ldx, void* Y,
+                                    coded_dtype y_dt, void* workspace, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (coded_status st = check_ar(q, r, lda)) return st;
+    if (s < 0) return fail(CODED_ERR_SHAPE, "s must be >= 0");
+    if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
+    if (block_rows(q, c->k) * s > 0 && r > 0 && (!X || !Y)) return fail(CODED_ERR_ARG, "X or Y is NULL");
+    if (dt == CODED_BF16 && !workspace && block_rows(q, c->k) * s > 0 && r > 0)
+        return fail(CODED_ERR_ARG, "bf16 needs the worker workspace");
+    return do_encode_workers(c, dt, A, q, r, lda, parity, X, s, ldx, Y, y_dt, workspace,
+                             static_cast<hipStream_t>(stream));
     CODED_GUARD_END
 }
 
@@ -402,10 +490,13 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     if (s == 1 && ldx != 1 && dt == CODED_F32) return fail(CODED_ERR_UNSUPPORTED, "s == 1 needs ldx == 1");
     if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
 
-    if (!parity_ready)
-        if (coded_status s2 = do_encode(c, dt, A, q, r, lda, parity, st)) return s2;
     void* wws = static_cast<char*>(workspace) + matmul_y_bytes(c, dt, q, s);
-    if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, workspace, y_dt, wws, st)) return s2;
+    if (!parity_ready) {
+        if (coded_status s2 = do_encode_workers(c, dt, A, q, r, lda, parity, X, s, ldx, workspace, y_dt, wws, st))
+            return s2;
+    } else if (coded_status s2 = do_workers(c, dt, A, q, r, lda, parity, X, s, ldx, nullptr, workspace, y_dt, wws, st)) {
+        return s2;
+    }
     if (coded_status s2 = do_decode_single(c, set, m, workspace, y_dt, q, s, out, ldo, info, st)) return s2;
     if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
     if (t_overall_out) *t_overall_out = t;

@@ -13,7 +13,9 @@ struct coded_code {
     int32_t n = 0, k = 0, planes = 2;
     std::vector<double> G;     // host copy, n*k row-major
     double* dG = nullptr;      // device copy, n*k row-major
+    float* dPf = nullptr;      // device copy of the parity rows P ((n-k) x k) in fp32
     int device = 0;
+    int compute_units = 0;     // of the device, for kernels that place one workgroup per unit
     // Created on first use by coded_straggler_matmul, released with the code:
     // default-priority streams the worker products run on, one completion
     // event per worker, and an event that orders them after the caller.
@@ -64,6 +66,20 @@ hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
 hipError_t launch_transpose_x_bf16(const WorkerArgs& a, hipStream_t st);
 // Bytes of the bf16 worker workspace (X transposed), 256-byte aligned.
 int64_t worker_workspace_bytes_bf16(int64_t r, int64_t s);
+
+// ---------------------------------------------------------------- fused encode + workers (bf16)
+struct FusedArgs {
+    const uint16_t* A;    // q x r bf16, row stride lda
+    uint16_t* parity;     // 2 planes x (n-k) x qb x r, written
+    const uint16_t* xt;   // X^T, s x r (s = 64)
+    float* Y;             // n x qb x 64, written (zero-filled, then accumulated)
+    const float* P;       // device (n-k) x k parity coefficients (bf16 values)
+    int64_t q, r, lda, qb;
+    int32_t n, k;
+    int64_t stages = 0, units = 0, per = 0, clean_tiles = 0;   // set by the launcher
+};
+bool fused_bf16_supported(int n, int k, int planes, int64_t r, int64_t lda);
+hipError_t launch_fused_bf16(FusedArgs a, bool products, int compute_units, hipStream_t st);
 
 // ---------------------------------------------------------------- decode
 // One survivor set passed by value (worker indices < 128 fit in a byte;
