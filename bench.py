@@ -53,15 +53,21 @@ def kernel_source_hash(sources=None) -> str:
     return h.hexdigest()
 
 
-def measured_traffic(per_launch_algorithmic: float):
-    """HBM bytes per GEMV launch from the committed rocprofv3 counter summary,
-    or None when it is missing or was taken on a different kernel source."""
+# Single-pass bf16 encode + worker products: the same kind of summary.
+DENSE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_traffic_dense32x24.json")
+DENSE_SOURCES = ["paper_1512_02673_amd/csrc/fused_bf16.hip", "paper_1512_02673_amd/csrc/internal.h"]
+
+
+def measured_traffic(per_launch_algorithmic: float, path=TRAFFIC_FILE, sources=None):
+    """HBM bytes per launch of a kernel from a committed rocprofv3 counter
+    summary, or None when it is missing or was taken on a different kernel
+    source (the GEMV's by default)."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash():
+    if t.get("kernel_source_sha256") != kernel_source_hash(sources):
         return None
     if abs(float(t.get("algorithmic_bytes_per_launch", -1.0)) - per_launch_algorithmic) > 1.0:
         return None                      # counters of another launch shape
@@ -514,7 +520,8 @@ def dense_bf16_workload(args):
         "roofline": {"bound": "hbm", "kernel": "fused_bf16_kernel (with the X transpose and the Y zero fill)",
                      "achieved": fused_bytes / (fused_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                     "algorithmic_bytes_per_launch": fused_bytes, "traffic": None,
+                     "algorithmic_bytes_per_launch": fused_bytes,
+                     "traffic": measured_traffic(fused_bytes, DENSE_TRAFFIC_FILE, DENSE_SOURCES),
                      "mfma_tflops": (wrk_flops + enc_flops) / (fused_ms * 1e-3) / 1e12,
                      "mfma_frac_of_bf16_dense_peak": (wrk_flops + enc_flops) / (fused_ms * 1e-3) / 2.5e15,
                      "mfma_ceiling_at_hbm_peak": (wrk_flops + enc_flops) / (fused_bytes / 8e12) / 2.5e15},
