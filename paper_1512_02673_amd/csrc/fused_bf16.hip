@@ -105,10 +105,21 @@ __global__ __launch_bounds__(WAVES * 64, 1) void fused_bf16_kernel(FusedArgs a) 
         }
         cur_tile = tile;
     };
-    auto load = [&](int set, int64_t u) __attribute__((always_inline)) {
-        const int64_t tile = u / a.stages;
+    // (tile, stage) of a unit, advanced one unit at a time (no division in the loop)
+    const int nst = static_cast<int>(a.stages);
+    struct Cursor {
+        int tile, s;
+    };
+    auto advance = [&](Cursor& c) __attribute__((always_inline)) {
+        if (++c.s == nst) {
+            c.s = 0;
+            ++c.tile;
+        }
+    };
+    auto load = [&](int set, const Cursor& cu) __attribute__((always_inline)) {
+        const int64_t tile = cu.tile;
         if (tile != cur_tile) set_tile(tile);
-        const int64_t kc = (u % a.stages) * kStage;
+        const int64_t kc = cu.s * kStage;
 #pragma unroll
         for (int i = 0; i < AP; ++i) ar[set][i] = *reinterpret_cast<const u32x4f*>(a.A + aoff[i] + kc);
         if constexpr (PRODUCTS) {
@@ -121,10 +132,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void fused_bf16_kernel(FusedArgs a) 
         }
     };
 
+    Cursor cc{static_cast<int>(u0 / a.stages), static_cast<int>(u0 % a.stages)};   // the unit being computed
+    Cursor cl = cc;                              // the unit being loaded
     auto body = [&](int set, int64_t u) __attribute__((always_inline)) {
         const int b = set;
-        const int64_t tile = u / a.stages;
-        const int64_t s = u % a.stages;
+        const int64_t tile = cc.tile;
+        const int64_t s = cc.s;
         const int64_t t0 = tile * 16;
         const bool masked = tile >= a.clean_tiles;
         // stage u into LDS (padding rows as zeros), then start the loads of u + 2
@@ -145,7 +158,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void fused_bf16_kernel(FusedArgs a) 
                 sX[b][swz(e >> 3, e & 7)] = xr[set][i];
             }
         }
-        load(set, min<int64_t>(u + 2, u1 - 1));
+        if (u + 2 < u1) advance(cl);             // else the last unit is loaded again
+        load(set, cl);
         __syncthreads();
 
         // encode: column groups g of this wave; lane (li, lk) reads blocks 8 lk .. 8 lk + 7
@@ -263,10 +277,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void fused_bf16_kernel(FusedArgs a) 
                 zero_acc();
             }
         }
+        advance(cc);
     };
 
-    load(0, u0);
-    load(1, min<int64_t>(u0 + 1, u1 - 1));
+    load(0, cl);
+    if (u0 + 1 < u1) advance(cl);
+    load(1, cl);
     for (int64_t u = u0; u < u1; u += 2) {
         body(0, u);
         if (u + 1 < u1) body(1, u + 1);
