@@ -73,6 +73,8 @@ def test_host_argument_errors(lib):
     assert h.coded_code_create(4, 2, np.eye(4, 2).ctypes.data, 3, ctypes.byref(ctypes.c_void_p())) == \
         lib.CODED_ERR_ARG
     assert h.coded_encode(None, 0, None, 0, 0, 1, None, None) == lib.CODED_ERR_ARG
+    assert h.coded_encode_worker_mm(None, 1, None, 0, 0, 1, None, None, 0, 1, None, 0, None, None) == \
+        lib.CODED_ERR_ARG
     assert h.coded_decode(None, None, 0, None, 2, 0, 0, None, 1, None, None) == lib.CODED_ERR_ARG
     assert h.coded_straggler_matmul(None, 0, None, 0, 0, 1, None, None, 1, 1, 0, 0, 1.0, 1.0, 1.0, 0, None, 2, None,
                                     None, 1, None, None, None, None, None) == lib.CODED_ERR_ARG

@@ -147,3 +147,33 @@ def test_matmul_single_pass_end_to_end(lib, torch):
     lib.coded_encode(code, dA, par_e)
     torch.cuda.synchronize()
     assert torch.equal(par.view(torch.int16), par_e.view(torch.int16))
+
+
+def test_single_pass_argument_errors(lib, torch):
+    """Bad arguments are refused on the host before anything is enqueued."""
+    import ctypes
+    q, r, s = 100, 64, 64
+    P, A, X = make_inputs(N, K, q, r, s, 36, "bf16")
+    code = lib.Code.systematic(P, 2)
+    dA, dX = device_tensor(A, "bf16"), device_tensor(X, "bf16")
+    par = lib.alloc_parity(code, q, r, torch.bfloat16)
+    Y = lib.alloc_y(code, q, s, torch.float32)
+    h, vp = lib.lib(), ctypes.c_void_p
+    st = vp(torch.cuda.current_stream().cuda_stream)
+    ws = lib.worker_workspace(code, dA, dX)
+    args = [code.handle, lib.CODED_BF16, vp(dA.data_ptr()), q, r, r, vp(par.data_ptr()), vp(dX.data_ptr()), s, s,
+            vp(Y.data_ptr()), lib.CODED_F32, vp(ws.data_ptr()), st]
+    assert h.coded_encode_worker_mm(*args) == lib.CODED_OK
+    bad = list(args)
+    bad[12] = None                                  # bf16 needs the workspace
+    assert h.coded_encode_worker_mm(*bad) == lib.CODED_ERR_ARG
+    bad = list(args)
+    bad[11] = lib.CODED_F64                         # bf16 products are fp32
+    assert h.coded_encode_worker_mm(*bad) == lib.CODED_ERR_ARG
+    bad = list(args)
+    bad[9] = s - 1                                  # ldx < s
+    assert h.coded_encode_worker_mm(*bad) == lib.CODED_ERR_SHAPE
+    bad = list(args)
+    bad[5] = r - 1                                  # lda < r
+    assert h.coded_encode_worker_mm(*bad) == lib.CODED_ERR_SHAPE
+    torch.cuda.synchronize()
