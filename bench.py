@@ -74,6 +74,26 @@ def measured_traffic(per_launch_algorithmic: float, path=TRAFFIC_FILE, sources=N
     return float(t["hbm_bytes_per_launch"])
 
 
+def measured_kernel_traffic(workload: str, kernel: str, per_launch_algorithmic: float):
+    """HBM bytes per launch of one kernel of a workload from its committed
+    rocprofv3 summary (profiles/traffic_<workload>.json), or None when it is
+    missing, was taken on different kernel sources, or on another launch shape."""
+    try:
+        with open(os.path.join(ROOT, "profiles", f"traffic_{workload}.json")) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash(t.get("sources")):
+        return None
+    kt = t.get("kernels", {}).get(kernel)
+    if not kt:
+        return None
+    alg = float(kt.get("algorithmic_bytes_per_launch", -1.0))
+    if abs(alg - per_launch_algorithmic) > 1e-9 * max(alg, 1.0) + 1.0:
+        return None
+    return float(kt["hbm_bytes_per_launch"])
+
+
 def measured_valu(draws: int):
     """Executed VALU wave-instructions per runtime-model launch of `draws`
     draws, or None when the summary is missing or for another source."""
@@ -213,7 +233,10 @@ def gemv_workload(args):
     algo_bytes = 4.0 * q * r + 4.0 * code.planes * (n - k) * qb * r + 4.0 * r + 8.0 * n * qb
     gemv_mean_ms = float(gemv_ms.mean())
     achieved = algo_bytes / (gemv_mean_ms * 1e-3) / 1e9
-    traffic = measured_traffic(algo_bytes)
+    if w.name == "gemv16x12_65536x8192":
+        traffic = measured_traffic(algo_bytes)
+    else:
+        traffic = measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 8, 256>", algo_bytes)
     result = {
         "metric": METRIC,
         "value": K / elapsed,
@@ -431,7 +454,7 @@ def decode_workload(args):
                    "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean())},
         "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
-                     "traffic": None, "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12},
+                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)
@@ -532,7 +555,9 @@ def gd_workload(args):
         "step_ms_events": step_ms, "gemv_A_ms": tA, "gemv_AT_ms": tT,
         "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel (A and A^T launches)", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "algorithmic_bytes_per_launch": [bA, bT], "traffic": None,
+                     "algorithmic_bytes_per_launch": [bA, bT],
+                     "traffic": [measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 4, 256>", bA),
+                                 measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 8, 256>", bT)],
                      "step_frac": (bA + bT) / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
     }
     return result
@@ -865,7 +890,9 @@ def shuffle_workload(args):
         "encode_ms": enc_ms, "decode_ms": dec_ms,
         "roofline": {"bound": "hbm", "kernel": "shuffle_decode_kernel", "achieved": dec_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": dec_gbs / HBM_PEAK_GBS,
-                     "algorithmic_bytes_per_launch": float(a[:, 7].mean()), "traffic": None,
+                     "algorithmic_bytes_per_launch": float(a[:, 7].mean()),
+                     "traffic": measured_kernel_traffic("shuffle16_1000000x256", "shuffle_decode_kernel<4>",
+                                                        float(a[:, 7].mean())),
                      "encode_achieved_gbs": enc_gbs, "encode_algorithmic_bytes_per_launch": float(a[:, 6].mean())},
     }
     if not args.no_cpu_baseline:
