@@ -432,9 +432,9 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
 }
 
 // One workgroup per (set, chunk): after the elimination its four waves copy
-// the systematic survivors, then combine the missing blocks on the matrix
-// cores; the workgroups resident on a compute unit drift apart in phase, so
-// copies and matrix-core work overlap across them.
+// the systematic survivors, then combine the missing blocks on the fp64
+// matrix cores (the combination is bound by their issue rate; the copy by
+// HBM writes).
 // KS: matrix-core K steps (4 survivors each) the kernel is built for, k <= 4 KS.
 template <int KS, int E, typename YT>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
