@@ -180,3 +180,27 @@ def test_single_pass_argument_errors(lib, torch):
     bad[5] = r - 1                                  # lda < r
     assert h.coded_encode_worker_mm(*bad) == lib.CODED_ERR_SHAPE
     torch.cuda.synchronize()
+
+
+def test_single_pass_strided_a(lib, torch):
+    """A with a row stride above r (a column window of a wider matrix): the
+    single pass reads it through lda, equal to the contiguous copy's results."""
+    q, r, s, pad = 2000, 256, 64, 64
+    P, A, X = make_inputs(N, K, q, r, s, 37, "bf16", integer=True)
+    code = lib.Code.systematic(P, 2)
+    wide = np.zeros((q, r + pad), dtype=np.float32)
+    wide[:, :r] = A
+    dW = device_tensor(wide, "bf16")
+    dA_view = dW[:, :r]                        # lda = r + pad
+    dA, dX = device_tensor(A, "bf16"), device_tensor(X, "bf16")
+    par_v = lib.alloc_parity(code, q, r, torch.bfloat16)
+    par_c = lib.alloc_parity(code, q, r, torch.bfloat16)
+    Yv = lib.alloc_y(code, q, s, torch.float32)
+    Yc = lib.alloc_y(code, q, s, torch.float32)
+    lib.coded_encode_worker_mm(code, dA_view, par_v, dX, Yv)
+    lib.coded_encode_worker_mm(code, dA, par_c, dX, Yc)
+    torch.cuda.synchronize()
+    assert torch.equal(par_v.view(torch.int16), par_c.view(torch.int16))
+    assert torch.equal(Yv, Yc)
+    ref = oc.encode(oc.systematic_generator(P), oc.pad_and_split(A, K))
+    assert np.array_equal(Yv.cpu().numpy().astype(np.float64), oc.worker_products(ref, X))
