@@ -94,6 +94,27 @@ def measured_kernel_traffic(workload: str, kernel: str, per_launch_algorithmic: 
     return float(kt["hbm_bytes_per_launch"])
 
 
+def measured_mfma(workload: str, kernel: str):
+    """Matrix-core counters of one kernel of a workload from its committed
+    rocprofv3 summary (profiles/mfma_<workload>.json): flops issued per launch
+    (SQ_INSTS_VALU_MFMA_MOPS_* x 512) and the busy fraction of the matrix
+    cores at the clock the launch ran at (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE per XCC x SIMDs).  None when missing or taken on other
+    kernel sources."""
+    try:
+        with open(os.path.join(ROOT, "profiles", f"mfma_{workload}.json")) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash(t.get("sources")):
+        return None
+    kt = t.get("kernels", {}).get(kernel)
+    if not kt:
+        return None
+    return {"kernel": kernel, "issued_flops_per_launch": kt["issued_flops_per_dispatch"],
+            "busy_frac": kt["mfma_util"]}
+
+
 def measured_valu(draws: int):
     """Executed VALU wave-instructions per runtime-model launch of `draws`
     draws, or None when the summary is missing or for another source."""
@@ -454,7 +475,8 @@ def decode_workload(args):
                    "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean())},
         "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
-                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12},
+                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
+                     "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double>")},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)
@@ -654,7 +676,8 @@ def dense_bf16_workload(args):
                      "traffic": measured_traffic(fused_bytes, DENSE_TRAFFIC_FILE, DENSE_SOURCES),
                      "mfma_tflops": (wrk_flops + enc_flops) / (fused_ms * 1e-3) / 1e12,
                      "mfma_frac_of_bf16_dense_peak": (wrk_flops + enc_flops) / (fused_ms * 1e-3) / 2.5e15,
-                     "mfma_ceiling_at_hbm_peak": (wrk_flops + enc_flops) / (fused_bytes / 8e12) / 2.5e15},
+                     "mfma_ceiling_at_hbm_peak": (wrk_flops + enc_flops) / (fused_bytes / 8e12) / 2.5e15,
+                     "mfma_counters": measured_mfma(w.name, "fused_bf16_kernel<8, 24, 8, true>")},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_dense(w, A, Xs, P, W, out, code.qb(q), args.cpu_rows)
