@@ -230,8 +230,15 @@ coded_status coded_draw_survivor_sets(int32_t n, int32_t k, uint64_t seed, uint6
  *   parity      device parity buffer; written first when parity_ready == 0.
  *   seed, draw, shift, rate   as coded_draw_survivors.
  *   survivors_out  host int32[k] (may be NULL); t_overall_out may be NULL.
- *   workspace   device, coded_sizes' workspace_bytes.
+ *   workspace   device, coded_sizes' workspace_bytes; holds every worker's
+ *               result Y (n x qb x s) when the call completes.
  *   info        device int32[1], as coded_decode.
+ * Small fp32 problems with one column (n <= 16, q*r <= 2^22, r and lda
+ * multiples of 4, A, parity and X 16-byte aligned) run as one launch: each
+ * block row's parity rows, products and decoded outputs are formed together,
+ * since block row t of every step depends on block row t of the data only.
+ * The planes written equal coded_encode's; results agree with the separate
+ * steps to fp64 summation order.
  */
 coded_status coded_matmul(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r, int64_t lda,
                           void* parity, int32_t parity_ready, const void* X, int64_t s, int64_t ldx, uint64_t seed,

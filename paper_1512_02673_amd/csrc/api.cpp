@@ -491,6 +491,33 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
 
     void* wws = static_cast<char*>(workspace) + matmul_y_bytes(c, dt, q, s);
+    if (dt == CODED_F32 && s == 1 && ldx == 1 && c->n > c->k && A && X && parity &&
+        onepass_supported(c->n, c->k, q, r, lda, A, parity, X)) {
+        // small problem: encode (unless ready), products and decode in one launch
+        OnePassArgs oa{};
+        oa.A = static_cast<const float*>(A);
+        oa.parity = static_cast<float*>(parity);
+        oa.x = static_cast<const float*>(X);
+        oa.Y = static_cast<double*>(workspace);
+        oa.out = out;
+        oa.info = info;
+        oa.G = c->dG;
+        oa.set = set;
+        oa.q = q;
+        oa.r = r;
+        oa.lda = lda;
+        oa.qb = qb;
+        oa.ldo = ldo;
+        oa.n = c->n;
+        oa.k = c->k;
+        oa.planes = c->planes;
+        oa.encode = parity_ready ? 0 : 1;
+        const hipError_t e = launch_onepass_f32(oa, st);
+        if (e != hipSuccess) return hip_fail(e, "one-pass product launch");
+        if (survivors_out) std::copy(surv, surv + c->k, survivors_out);
+        if (t_overall_out) *t_overall_out = t;
+        return CODED_OK;
+    }
     if (!parity_ready) {
         if (coded_status s2 = do_encode_workers(c, dt, A, q, r, lda, parity, X, s, ldx, workspace, y_dt, wws, st))
             return s2;
