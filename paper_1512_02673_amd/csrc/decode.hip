@@ -294,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
     if (!setup_set<kThreads>(a, single, b, writer, sm)) return;
     const int m = sm.m;
     const int first_par = k - m;
-    if (m > 0 && wv == 0) eliminate_wave(a, sm, m, first_par, lane, sD);
+    if (m > 0 && wv == 0) eliminate_set(a, sm, m, first_par, lane, sD);
     __syncthreads();
     if (sm.status != 0) {
         if (writer) a.info[b] = sm.status;

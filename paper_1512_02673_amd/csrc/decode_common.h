@@ -92,16 +92,20 @@ __device__ inline double lane_value(double v, int lane) {
     return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
 }
 
-// Wave-level elimination.  Lane l holds column l of the augmented matrix:
-// lanes < m the columns of G[S_par, M], lanes m..m+k-1 the right-hand sides
-// (sorted survivor order).  On success D[b][c] = sD[c * kFastLd + b] (rows
-// >= m zero); on a zero pivot sm.status = first_par + j + 1.
+// Wave-level elimination for sets with m <= MM <= kFastM.  Lane l holds
+// column l of the augmented matrix: lanes < m the columns of G[S_par, M],
+// lanes m..m+k-1 the right-hand sides (sorted survivor order).  On success
+// D[b][c] = sD[c * kFastLd + b] for b < kFastM (rows >= m zero); on a zero
+// pivot sm.status = first_par + j + 1.  The operations on rows < m do not
+// depend on MM, so every MM >= m gives the same D.
+template <int MM>
 __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm, int m, int first_par, int lane, double* sD) {
+    static_assert(MM <= kFastM, "MM");
     const int k = a.k;
     const int c = lane - m;
-    double col[kFastM];
+    double col[MM];
 #pragma unroll
-    for (int r = 0; r < kFastM; ++r) {
+    for (int r = 0; r < MM; ++r) {
         double v = 0.0;
         if (r < m) {
             const int64_t prow = static_cast<int64_t>(sm.S[first_par + r]) * k;
@@ -116,7 +120,7 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
     }
     int status = 0;
 #pragma unroll
-    for (int j = 0; j < kFastM; ++j) {
+    for (int j = 0; j < MM; ++j) {
         // uniform guards instead of an early exit keep the loop fully unrolled
         // (every register index a constant)
         if (j < m && status == 0) {
@@ -124,7 +128,7 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
             int p = j;
             double best = fabs(col[j]);
 #pragma unroll
-            for (int i = j + 1; i < kFastM; ++i) {
+            for (int i = j + 1; i < MM; ++i) {
                 const double v = fabs(col[i]);
                 if (i < m && v > best) {
                     best = v;
@@ -137,7 +141,7 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
                 status = first_par + j + 1;
             } else {
 #pragma unroll
-                for (int i = j + 1; i < kFastM; ++i) {
+                for (int i = j + 1; i < MM; ++i) {
                     if (i == p) {
                         const double t = col[i];
                         col[i] = col[j];
@@ -151,7 +155,7 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
                 const double piv = lane_value(col[j], j);
                 const double inv = 1.0 / piv;
 #pragma unroll
-                for (int i = 0; i < kFastM; ++i) {
+                for (int i = 0; i < MM; ++i) {
                     if (i != j && i < m) {
                         const double aij = lane_value(col[i], j);
                         const double l0 = aij * inv;
@@ -165,9 +169,20 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
     }
     if (status == 0 && c >= 0 && c < k) {
 #pragma unroll
-        for (int r = 0; r < kFastM; ++r) sD[c * kFastLd + r] = col[r];
+        for (int r = 0; r < kFastM; ++r) sD[c * kFastLd + r] = r < MM ? col[r] : 0.0;
     }
     if (lane == 0) sm.status = status;
+}
+
+// The smallest register size that holds a set with m missing blocks.
+__device__ __forceinline__ void eliminate_set(const DecodeArgs& a, SetMeta& sm, int m, int first_par, int lane,
+                                              double* sD) {
+    if (m <= 4)
+        eliminate_wave<4>(a, sm, m, first_par, lane, sD);
+    else if (m <= 8)
+        eliminate_wave<8>(a, sm, m, first_par, lane, sD);
+    else
+        eliminate_wave<kFastM>(a, sm, m, first_par, lane, sD);
 }
 
 }  // namespace

@@ -16,6 +16,7 @@
 // stored planes equal coded_encode's bit for bit.  Products are exact in
 // fp64 and summed in fp64.
 #include "internal.h"
+#include "onepass.h"
 #include "decode_common.h"
 #include "worker_common.h"
 
@@ -34,18 +35,40 @@ __device__ inline double dot4(f32x4o a, f32x4o x, double acc) {
     return acc;
 }
 
-template <int NT>
+// KM >= k: data rows held per thread (registers are sized by it).
+template <int NT, int KM>
 __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
     constexpr int NW = NT / 64;
     constexpr int MN = kOnePassMaxN;
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
-    __shared__ double sP[MN * MN];
     __shared__ double red[NW][MN];
     __shared__ double sy[MN];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int n = a.n, k = a.k, npar = n - k;
     const int64_t t = blockIdx.x;
+    int kin = 0;                                  // data blocks whose row t lies inside A
+    while (kin < k && static_cast<int64_t>(kin) * a.qb + t < a.q) ++kin;
+    int m0 = 0;                                   // missing blocks: survivors at or past k
+    for (int c = 0; c < k; ++c) m0 += set_entry(a.set, c) >= k ? 1 : 0;
+    // With blocks to solve for, wave 0 forms D while the other waves stream
+    // the columns (the two chains run side by side); otherwise all stream.
+    const int cw = (m0 > 0 && NW > 1) ? 1 : 0;
+
+    // This thread's first columns are requested before anything else, so the
+    // memory latency overlaps the set bookkeeping and the elimination.
+    auto load_chunk = [&](int64_t c, f32x4o (&av)[KM], f32x4o& xv) __attribute__((always_inline)) {
+        xv = load4(a.x + c);
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+            av[j] = f32x4o{0.f, 0.f, 0.f, 0.f};
+            if (j < kin) av[j] = load4(a.A + (static_cast<int64_t>(j) * a.qb + t) * a.lda + c);
+        }
+    };
+    f32x4o avA[KM], avB[KM], xA, xB;
+    const int64_t kStep = static_cast<int64_t>(NT - 64 * cw) * 4;
+    int64_t c = wv < cw ? a.r : static_cast<int64_t>(tid - 64 * cw) * 4;
+    if (c < a.r) load_chunk(c, avA, xA);
 
     DecodeArgs da{};
     da.G = a.G;
@@ -58,42 +81,32 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
     da.k = k;
     da.batch = 1;
     setup_set<NT>(da, a.set, 0, false, sm);     // the host has checked the set
-    for (int e = tid; e < npar * k; e += NT) sP[e] = a.G[static_cast<int64_t>(k) * k + e];
-    __syncthreads();
     const int m = sm.m;
-    if (m > 0 && wv == 0) eliminate_wave(da, sm, m, k - m, lane, sD);   // read after the barrier below
+    if (m > 0 && wv == 0) eliminate_set(da, sm, m, k - m, lane, sD);   // read after the barrier below
 
     // Row t of the data blocks (zero past q), the parity rows, and the n products.
     double y[MN];
 #pragma unroll
     for (int i = 0; i < MN; ++i) y[i] = 0.0;
-    int kin = 0;                                  // data blocks whose row t lies inside A
-    while (kin < k && static_cast<int64_t>(kin) * a.qb + t < a.q) ++kin;
     const int64_t plane = static_cast<int64_t>(npar) * a.qb * a.r;
-    for (int64_t c = static_cast<int64_t>(tid) * 4; c < a.r; c += NT * 4) {
-        const f32x4o xv = load4(a.x + c);
-        f32x4o av[MN];
+    auto process = [&](int64_t c, const f32x4o (&av)[KM], f32x4o xv) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < MN; ++j) {
-            av[j] = f32x4o{0.f, 0.f, 0.f, 0.f};
-            if (j < kin) av[j] = load4(a.A + (static_cast<int64_t>(j) * a.qb + t) * a.lda + c);
-        }
-#pragma unroll
-        for (int j = 0; j < MN; ++j)
+        for (int j = 0; j < KM; ++j)
             if (j < kin) y[j] = dot4(av[j], xv, y[j]);
         for (int p = 0; p < npar; ++p) {
             float* prow = a.parity + (static_cast<int64_t>(p) * a.qb + t) * a.r + c;
+            const double* g = a.G + static_cast<int64_t>(k + p) * k;    // parity row p of G (uniform)
             f32x4o hi, lo = f32x4o{0.f, 0.f, 0.f, 0.f};
             if (a.encode) {
                 double s4[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-                for (int j = 0; j < MN; ++j) {
+                for (int j = 0; j < KM; ++j) {
                     if (j < kin) {
-                        const double g = sP[p * k + j];
-                        s4[0] = fma(g, static_cast<double>(av[j].x), s4[0]);
-                        s4[1] = fma(g, static_cast<double>(av[j].y), s4[1]);
-                        s4[2] = fma(g, static_cast<double>(av[j].z), s4[2]);
-                        s4[3] = fma(g, static_cast<double>(av[j].w), s4[3]);
+                        const double gj = g[j];
+                        s4[0] = fma(gj, static_cast<double>(av[j].x), s4[0]);
+                        s4[1] = fma(gj, static_cast<double>(av[j].y), s4[1]);
+                        s4[2] = fma(gj, static_cast<double>(av[j].z), s4[2]);
+                        s4[3] = fma(gj, static_cast<double>(av[j].w), s4[3]);
                     }
                 }
                 hi = f32x4o{static_cast<float>(s4[0]), static_cast<float>(s4[1]), static_cast<float>(s4[2]),
@@ -117,6 +130,16 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
             for (int i = 0; i < MN; ++i)
                 if (i == k + p) y[i] += yp;
         }
+    };
+    // one chunk of loads in flight ahead of the chunk being combined
+    while (c < a.r) {
+        if (c + kStep < a.r) load_chunk(c + kStep, avB, xB);
+        process(c, avA, xA);
+        c += kStep;
+        if (c >= a.r) break;
+        if (c + kStep < a.r) load_chunk(c + kStep, avA, xA);
+        process(c, avB, xB);
+        c += kStep;
     }
 #pragma unroll
     for (int i = 0; i < MN; ++i) {
@@ -148,9 +171,19 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
         int b = 0;                               // rank of j among the missing blocks
         for (int i = 0; i < j; ++i) b += sm.present[i] ? 0 : 1;
         v = 0.0;
-        for (int c = 0; c < k; ++c) v = fma(sD[c * kFastLd + b], sy[sm.S[c]], v);
+        for (int c2 = 0; c2 < k; ++c2) v = fma(sD[c2 * kFastLd + b], sy[sm.S[c2]], v);
     }
     a.out[(static_cast<int64_t>(j) * a.qb + t) * a.ldo] = static_cast<float>(v);
+}
+
+template <int NT>
+void launch_nt(const OnePassArgs& a, dim3 grid, hipStream_t st) {
+    if (a.k <= 4)
+        hipLaunchKernelGGL((onepass_f32_kernel<NT, 4>), grid, dim3(NT), 0, st, a);
+    else if (a.k <= 8)
+        hipLaunchKernelGGL((onepass_f32_kernel<NT, 8>), grid, dim3(NT), 0, st, a);
+    else
+        hipLaunchKernelGGL((onepass_f32_kernel<NT, 16>), grid, dim3(NT), 0, st, a);
 }
 
 bool aligned16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -168,13 +201,15 @@ bool onepass_supported(int n, int k, int64_t q, int64_t r, int64_t lda, const vo
 hipError_t launch_onepass_f32(const OnePassArgs& a, hipStream_t st) {
     if (a.qb == 0) return hipSuccess;
     if (a.qb > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    // Wave 0 forms D while the others stream: one streaming wave per 256
+    // columns up to two, then three.
     const dim3 grid(static_cast<unsigned>(a.qb));
     if (a.r <= 256)
-        hipLaunchKernelGGL(onepass_f32_kernel<64>, grid, dim3(64), 0, st, a);
+        launch_nt<128>(a, grid, st);
     else if (a.r <= 512)
-        hipLaunchKernelGGL(onepass_f32_kernel<128>, grid, dim3(128), 0, st, a);
+        launch_nt<192>(a, grid, st);
     else
-        hipLaunchKernelGGL(onepass_f32_kernel<256>, grid, dim3(256), 0, st, a);
+        launch_nt<256>(a, grid, st);
     return hipGetLastError();
 }
 
