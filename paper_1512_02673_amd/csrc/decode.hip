@@ -286,6 +286,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
                                                                int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
+    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 256 : 1];   // per-wave output tile
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int k = a.k;
     const int64_t b = blockIdx.x / chunks;
@@ -363,7 +364,24 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
             const double bv = (valid >> st) & 1u ? static_cast<double>(yv[st]) : 0.0;
             acc = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], bv, acc, 0, 0, 0);
         }
-        if (e < e1) {
+        if constexpr (E == 4) {
+            // Through this wave's LDS tile (16 blocks x 16 elements, fp64) so
+            // that each lane writes 4 consecutive elements of one block with
+            // one 16-byte store: lane l takes block l / 4, elements
+            // 4 (l % 4) .. 4 (l % 4) + 3 of the tile.
+            double* buf = sOut[wv];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) buf[(4 * v + lk) * 16 + li] = acc[v];
+            const int bb = lane >> 2, eg = e0 + tile * 16 + 4 * (lane & 3);
+            if (bb < m && eg < e1) {
+                double v4[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v4[i] = buf[bb * 16 + 4 * (lane & 3) + i];
+                const int t = eg / s, col = eg - t * s;     // s % 4 == 0: the four share row t
+                const int w = sm.miss[bb];
+                if (t < sm.lim[w]) store_out<4>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, v4);
+            }
+        } else if (e < e1) {
             const int t = e / s, col = e - t * s;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
