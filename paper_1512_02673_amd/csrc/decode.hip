@@ -286,7 +286,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
                                                                int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
-    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 256 : 1];   // per-wave output tile
+    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 512 : 1];   // per-wave output tile
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int k = a.k;
     const int64_t b = blockIdx.x / chunks;
@@ -347,49 +347,81 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         yo[st] = c < k ? static_cast<int32_t>(sm.yoff[c]) : 0;
         valid |= (c < k ? 1u : 0u) << st;
     }
-    const int ntiles = (e1 - e0 + 15) / 16;
-    for (int tile = wv; tile < ntiles; tile += kWaves) {
-        const int e = e0 + tile * 16 + li;
-        // Straight-line loads, all issued before the first is used.  A lane
-        // past the chunk's end reads its last element instead: column li of
-        // the product depends on column li of Y only, and is not stored.
-        const int el = min(e, e1 - 1);
-        YT yv[KS];
+    if constexpr (E == 4) {
+        // Tiles in pairs: lane (li, lk) loads elements 2 li and 2 li + 1 of a
+        // 32-element pair with one load, and two matrix-core products take
+        // the even and the odd elements.  The results go through this wave's
+        // LDS tile (16 blocks x 32 elements, fp64) back into element order,
+        // and each lane writes 4 consecutive elements of one block with one
+        // 16-byte store.  (E == 4: s % 4 == 0 and Y, out 16-byte aligned, so
+        // the chunk bounds and the total are multiples of 4.)
+        typedef YT yt2 __attribute__((ext_vector_type(2)));
+        double* buf = sOut[wv];
+        const int npairs = (e1 - e0 + 31) / 32;
+        for (int pr = wv; pr < npairs; pr += kWaves) {
+            const int base = e0 + pr * 32;
+            // a pair past the chunk's end reads the block's last two elements
+            // instead (in bounds; those columns are not stored)
+            const int el = min(base + 2 * li, total - 2);
+            yt2 yv[KS];
 #pragma unroll
-        for (int st = 0; st < KS; ++st) yv[st] = Y[yo[st] + el];
-        f64x4v acc = {0.0, 0.0, 0.0, 0.0};
+            for (int st = 0; st < KS; ++st) yv[st] = *reinterpret_cast<const yt2*>(Y + yo[st] + el);
+            f64x4v acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int st = 0; st < KS; ++st) {
-            // padding steps (k not a multiple of 4) contribute exact zeros
-            const double bv = (valid >> st) & 1u ? static_cast<double>(yv[st]) : 0.0;
-            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], bv, acc, 0, 0, 0);
-        }
-        if constexpr (E == 4) {
-            // Through this wave's LDS tile (16 blocks x 16 elements, fp64) so
-            // that each lane writes 4 consecutive elements of one block with
-            // one 16-byte store: lane l takes block l / 4, elements
-            // 4 (l % 4) .. 4 (l % 4) + 3 of the tile.
-            double* buf = sOut[wv];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) buf[(4 * v + lk) * 16 + li] = acc[v];
-            const int bb = lane >> 2, eg = e0 + tile * 16 + 4 * (lane & 3);
-            if (bb < m && eg < e1) {
-                double v4[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) v4[i] = buf[bb * 16 + 4 * (lane & 3) + i];
-                const int t = eg / s, col = eg - t * s;     // s % 4 == 0: the four share row t
-                const int w = sm.miss[bb];
-                if (t < sm.lim[w]) store_out<4>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, v4);
+            for (int st = 0; st < KS; ++st) {
+                // padding steps (k not a multiple of 4) contribute exact zeros
+                const bool ok = (valid >> st) & 1u;
+                const double b0 = ok ? static_cast<double>(yv[st].x) : 0.0;
+                const double b1 = ok ? static_cast<double>(yv[st].y) : 0.0;
+                acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], b0, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], b1, acc1, 0, 0, 0);
             }
-        } else if (e < e1) {
-            const int t = e / s, col = e - t * s;
+            // item v of lane (li, lk): block 4 v + lk, elements 2 li (acc0) and 2 li + 1 (acc1)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int bb = 4 * v + lk;
-                if (bb < m) {
+                buf[(4 * v + lk) * 32 + 2 * li] = acc0[v];
+                buf[(4 * v + lk) * 32 + 2 * li + 1] = acc1[v];
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int bb = lane >> 2, g4 = (lane & 3) + 4 * h, eg = base + 4 * g4;
+                if (bb < m && eg < e1) {
+                    double v4[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v4[i] = buf[bb * 32 + 4 * g4 + i];
+                    const int t = eg / s, col = eg - t * s;     // s % 4 == 0: the four share row t
                     const int w = sm.miss[bb];
-                    const double val = acc[v];
-                    if (t < sm.lim[w]) store_out<1>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, &val);
+                    if (t < sm.lim[w]) store_out<4>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, v4);
+                }
+            }
+        }
+    } else {
+        const int ntiles = (e1 - e0 + 15) / 16;
+        for (int tile = wv; tile < ntiles; tile += kWaves) {
+            const int e = e0 + tile * 16 + li;
+            // Straight-line loads, all issued before the first is used.  A lane
+            // past the chunk's end reads its last element instead: column li of
+            // the product depends on column li of Y only, and is not stored.
+            const int el = min(e, e1 - 1);
+            YT yv[KS];
+#pragma unroll
+            for (int st = 0; st < KS; ++st) yv[st] = Y[yo[st] + el];
+            f64x4v acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+            for (int st = 0; st < KS; ++st) {
+                const double bv = (valid >> st) & 1u ? static_cast<double>(yv[st]) : 0.0;
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], bv, acc, 0, 0, 0);
+            }
+            if (e < e1) {
+                const int t = e / s, col = e - t * s;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int bb = 4 * v + lk;
+                    if (bb < m) {
+                        const int w = sm.miss[bb];
+                        const double val = acc[v];
+                        if (t < sm.lim[w]) store_out<1>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, &val);
+                    }
                 }
             }
         }
