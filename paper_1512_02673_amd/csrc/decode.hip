@@ -276,6 +276,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a, DecodeSe
 // on v_mfma_f64_16x16x4f64, with D held in registers for the whole set.
 typedef double f64x4v __attribute__((ext_vector_type(4)));
 
+// Consecutive elements per lane in the combination's loads (E == 4 path);
+// 4 needs 192 registers at k = 48 (2 waves per SIMD) and measured slower.
+constexpr int kDecodePE = 2;
+
+// PE consecutive elements of Y (16-byte aligned for fp64 pairs, PE * 4-byte
+// aligned for fp32) with vector loads.
+template <int PE, typename YT>
+__device__ inline void load_pe(const YT* p, YT (&v)[PE]) {
+    if constexpr (sizeof(YT) == 8) {
+#pragma unroll
+        for (int i = 0; i < PE; i += 2) {
+            const double2 d = reinterpret_cast<const double2*>(p)[i / 2];
+            v[i] = d.x;
+            v[i + 1] = d.y;
+        }
+    } else if constexpr (PE == 4) {
+        const float4 f = *reinterpret_cast<const float4*>(p);
+        v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    } else {
+        const float2 f = *reinterpret_cast<const float2*>(p);
+        v[0] = f.x; v[1] = f.y;
+    }
+}
+
 // One workgroup per (set, chunk): after the elimination its four waves copy
 // the systematic survivors, then combine the missing blocks on the fp64
 // matrix cores (the combination is bound by their issue rate; the copy by
@@ -286,7 +310,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
                                                                int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
-    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 512 : 1];   // per-wave output tile
+    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 256 * kDecodePE : 1];   // per-wave output tile
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int k = a.k;
     const int64_t b = blockIdx.x / chunks;
@@ -348,47 +372,49 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         valid |= (c < k ? 1u : 0u) << st;
     }
     if constexpr (E == 4) {
-        // Tiles in pairs: lane (li, lk) loads elements 2 li and 2 li + 1 of a
-        // 32-element pair with one load, and two matrix-core products take
-        // the even and the odd elements.  The results go through this wave's
-        // LDS tile (16 blocks x 32 elements, fp64) back into element order,
-        // and each lane writes 4 consecutive elements of one block with one
-        // 16-byte store.  (E == 4: s % 4 == 0 and Y, out 16-byte aligned, so
-        // the chunk bounds and the total are multiples of 4.)
-        typedef YT yt2 __attribute__((ext_vector_type(2)));
+        // Tiles in groups of PE: lane (li, lk) loads elements PE li .. PE li +
+        // PE - 1 of a 16 PE-element group at once, and PE matrix-core
+        // products take the elements in each phase.  The results go through
+        // this wave's LDS tile (16 blocks x 16 PE elements, fp64) back into
+        // element order, and each lane writes 4 consecutive elements of one
+        // block per 16-byte store.  (E == 4: s % 4 == 0 and Y, out 16-byte
+        // aligned, so the chunk bounds and the total are multiples of 4.)
+        constexpr int PE = kDecodePE;
+        constexpr int W = 16 * PE;
         double* buf = sOut[wv];
-        const int npairs = (e1 - e0 + 31) / 32;
-        for (int pr = wv; pr < npairs; pr += kWaves) {
-            const int base = e0 + pr * 32;
-            // a pair past the chunk's end reads the block's last two elements
+        const int ngroups = (e1 - e0 + W - 1) / W;
+        for (int gp = wv; gp < ngroups; gp += kWaves) {
+            const int base = e0 + gp * W;
+            // a group past the chunk's end reads the block's last PE elements
             // instead (in bounds; those columns are not stored)
-            const int el = min(base + 2 * li, total - 2);
-            yt2 yv[KS];
+            const int el = min(base + PE * li, total - PE);
+            YT yv[KS][PE];
 #pragma unroll
-            for (int st = 0; st < KS; ++st) yv[st] = *reinterpret_cast<const yt2*>(Y + yo[st] + el);
-            f64x4v acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+            for (int st = 0; st < KS; ++st) load_pe<PE>(Y + yo[st] + el, yv[st]);
+            f64x4v acc[PE];
+#pragma unroll
+            for (int q = 0; q < PE; ++q) acc[q] = f64x4v{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int st = 0; st < KS; ++st) {
                 // padding steps (k not a multiple of 4) contribute exact zeros
                 const bool ok = (valid >> st) & 1u;
-                const double b0 = ok ? static_cast<double>(yv[st].x) : 0.0;
-                const double b1 = ok ? static_cast<double>(yv[st].y) : 0.0;
-                acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], b0, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], b1, acc1, 0, 0, 0);
-            }
-            // item v of lane (li, lk): block 4 v + lk, elements 2 li (acc0) and 2 li + 1 (acc1)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                buf[(4 * v + lk) * 32 + 2 * li] = acc0[v];
-                buf[(4 * v + lk) * 32 + 2 * li + 1] = acc1[v];
+                for (int q = 0; q < PE; ++q)
+                    acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], ok ? static_cast<double>(yv[st][q]) : 0.0,
+                                                                  acc[q], 0, 0, 0);
             }
+            // item v of lane (li, lk): block 4 v + lk, element PE li + q of acc[q]
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int q = 0; q < PE; ++q) buf[(4 * v + lk) * W + PE * li + q] = acc[q][v];
+#pragma unroll
+            for (int h = 0; h < PE; ++h) {
                 const int bb = lane >> 2, g4 = (lane & 3) + 4 * h, eg = base + 4 * g4;
                 if (bb < m && eg < e1) {
                     double v4[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v4[i] = buf[bb * 32 + 4 * g4 + i];
+                    for (int i = 0; i < 4; ++i) v4[i] = buf[bb * W + 4 * g4 + i];
                     const int t = eg / s, col = eg - t * s;     // s % 4 == 0: the four share row t
                     const int w = sm.miss[bb];
                     if (t < sm.lim[w]) store_out<4>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, v4);
