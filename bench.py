@@ -174,81 +174,70 @@ def gemv_workload(args):
     torch.cuda.synchronize()
     encode_ms = e0.elapsed_time(e1)
 
-    # The step calls the C ABI directly with arguments converted once, so that
-    # Python overhead stays far below the GPU time of a step.  Consecutive
-    # products are pipelined the way a master would run them: the workers of
-    # product t+1 run on `stream` while the decode of product t runs on a second
-    # stream (both default priority), with the worker results double-buffered
-    # and the two streams ordered by events.
+    # One step is one coded_matmul call (survivor draw, all n worker products,
+    # decode), made through the C ABI with its arguments converted once, so
+    # that Python overhead stays far below the GPU time of a step.  The timed
+    # loop records no per-step events: timing events and cross-stream waits
+    # between the workers and the decode measured about 12 us per product
+    # (2%), and a two-stream pipeline of workers and decode gained nothing
+    # over the calls back to back.
     import ctypes
     h = lib.lib()
     vp = ctypes.c_void_p
-    dec_stream = torch.cuda.Stream()
-    Ys = [Y, lib.alloc_y(code, q, 1, torch.float64)]
-    code_h, st_h, dst_h = code.handle, vp(stream.cuda_stream), vp(dec_stream.cuda_stream)
+    ws = lib.matmul_workspace(code, dA, dX[0])
+    code_h, st_h, ws_p = code.handle, vp(stream.cuda_stream), vp(ws.data_ptr())
     A_p, par_p = vp(dA.data_ptr()), vp(par.data_ptr())
-    Y_p = [vp(y.data_ptr()) for y in Ys]
     x_p = [vp(dX[t].data_ptr()) for t in range(K + W)]
     out_p = [vp(out[t].data_ptr()) for t in range(K + W)]
     info_p = [vp(info[t:t + 1].data_ptr()) for t in range(K + W)]
-    survs = [np.zeros(k, dtype=np.int32) for _ in range(2)]
-    surv_p = [sv.ctypes.data_as(vp) for sv in survs]
-    worked = [torch.cuda.Event() for _ in range(2)]      # worker results of buffer b are complete
-    decoded = [torch.cuda.Event() for _ in range(2)]     # decode of buffer b has read it
+    tk = ctypes.c_double()
+    tk_p = ctypes.addressof(tk)
 
-    def step(t, ev=None):
-        b = t % 2
-        rc = h.coded_draw_survivors(n, k, seed, t, 1.0, 1.0, surv_p[b], None)
-        stream.wait_event(decoded[b])
-        if ev is not None:
-            ev[0].record(stream)
-        rc |= h.coded_worker_mm(code_h, lib.CODED_F32, A_p, q, r, r, par_p, x_p[t], 1, 1, None, Y_p[b],
-                                lib.CODED_F64, None, st_h)
-        if ev is not None:
-            ev[1].record(stream)
-        worked[b].record(stream)
-        dec_stream.wait_event(worked[b])
-        if ev is not None:
-            ev[2].record(dec_stream)
-        rc |= h.coded_decode(code_h, surv_p[b], k, Y_p[b], lib.CODED_F64, q, 1, out_p[t], 1, info_p[t], dst_h)
-        if ev is not None:
-            ev[3].record(dec_stream)
-        decoded[b].record(dec_stream)
+    def step(t):
+        rc = h.coded_matmul(code_h, lib.CODED_F32, A_p, q, r, r, par_p, 1, x_p[t], 1, 1, seed, t, 1.0, 1.0, None,
+                            tk_p, out_p[t], 1, ws_p, info_p[t], st_h)
         if rc:
             raise RuntimeError(lib.last_error())
 
     for t in range(W):
         step(t)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    torch.cuda.synchronize()
     start = time.perf_counter()
     for i in range(K):
-        step(W + i, evs[i])
+        step(W + i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - start
     if int(info.abs().sum().item()) != 0:
         raise RuntimeError("a decode reported a singular or invalid survivor set")
-    gemv_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    dec_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
 
-    # The one-call entry point runs the same kernels: check it reproduces the
-    # decomposed step bit for bit, and time it.
-    ws = lib.alloc_y(code, q, 1, torch.float64)
+    # Per-kernel times, in a separate pass: the same products as separate
+    # worker and decode calls with events around each (these also check that
+    # coded_matmul equals the decomposed step bit for bit).
+    m_steps = min(K, 200)
+    Y2 = lib.alloc_y(code, q, 1, torch.float64)
     one = torch.empty(q, dtype=torch.float32, device="cuda")
     inf1 = torch.zeros(1, dtype=torch.int32, device="cuda")
-    for t in (W, W + K - 1):
-        lib.coded_matmul(code, dA, par, dX[t], one, ws, inf1, seed, t)
-        torch.cuda.synchronize()
-        if not torch.equal(one, out[t]):
-            raise RuntimeError("coded_matmul differs from the decomposed step")
-    m_steps = min(K, 200)
-    torch.cuda.synchronize()
-    tm = time.perf_counter()
+    surv = np.zeros(k, dtype=np.int32)
+    surv_p = surv.ctypes.data_as(vp)
+    Y2_p, one_p, inf1_p = vp(Y2.data_ptr()), vp(one.data_ptr()), vp(inf1.data_ptr())
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(m_steps)]
     for i in range(m_steps):
-        lib.coded_matmul(code, dA, par, dX[W + i], one, ws, inf1, seed, W + i)
+        t = W + i
+        h.coded_draw_survivors(n, k, seed, t, 1.0, 1.0, surv_p, None)
+        evs[i][0].record(stream)
+        h.coded_worker_mm(code_h, lib.CODED_F32, A_p, q, r, r, par_p, x_p[t], 1, 1, None, Y2_p, lib.CODED_F64, None,
+                          st_h)
+        evs[i][1].record(stream)
+        h.coded_decode(code_h, surv_p, k, Y2_p, lib.CODED_F64, q, 1, one_p, 1, inf1_p, st_h)
+        evs[i][2].record(stream)
+        if i in (0, m_steps - 1):
+            torch.cuda.synchronize()
+            if not torch.equal(one, out[t]):
+                raise RuntimeError("coded_matmul differs from the decomposed step")
     torch.cuda.synchronize()
-    matmul_ms = (time.perf_counter() - tm) * 1e3 / m_steps
+    gemv_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    dec_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    matmul_ms = elapsed * 1e3 / K
 
     qb = code.qb(q)
     algo_bytes = 4.0 * q * r + 4.0 * code.planes * (n - k) * qb * r + 4.0 * r + 8.0 * n * qb
@@ -540,17 +529,15 @@ def gd_workload(args):
     for t in range(W):
         lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, t, ws, info)
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    # no per-step events in the timed loop (they add GPU-side markers)
     start = time.perf_counter()
     for i in range(K):
-        evs[i][0].record(stream)
         lib.coded_gd_step(cA, cT, dA, pA, dAT, pT, dy, x, eta, seed, W + i, ws, info)
-        evs[i][1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - start
     if int(info.abs().sum().item()) != 0:
         raise RuntimeError("a decode reported a singular or invalid survivor set")
-    step_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    step_ms = elapsed * 1e3 / K
     # The two worker GEMV launches of a step, timed alone on the same buffers.
     Y1 = lib.alloc_y(cA, q, 1, torch.float64)
     Y2 = lib.alloc_y(cT, r, 1, torch.float64)
@@ -576,7 +563,7 @@ def gd_workload(args):
         "dtype": "f64", "data": "synthetic",
         "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "eta_applied": eta,
                    "codes": "separate (20,16) systematic codes for A and A^T, hi+lo parity"},
-        "step_ms_events": step_ms, "gemv_A_ms": tA, "gemv_AT_ms": tT,
+        "gemv_A_ms": tA, "gemv_AT_ms": tT,
         "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel (A and A^T launches)", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "algorithmic_bytes_per_launch": [bA, bT],
