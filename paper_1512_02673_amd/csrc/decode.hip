@@ -319,14 +319,6 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
     if (!setup_set<kThreads>(a, single, b, writer, sm)) return;
     const int m = sm.m;
     const int first_par = k - m;
-    if (m > 0 && wv == 0) eliminate_set(a, sm, m, first_par, lane, sD);
-    __syncthreads();
-    if (sm.status != 0) {
-        if (writer) a.info[b] = sm.status;
-        return;
-    }
-    if (writer) a.info[b] = 0;
-
     const YT* Y = static_cast<const YT*>(a.Y);
     float* out = a.out + b * a.out_stride;
     const int s = static_cast<int>(a.s);
@@ -335,11 +327,65 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
     const int e1 = min(total, e0 + elems_per_block);
     constexpr int kWaves = kThreads / 64;
 
-    // Systematic survivors: U survivors' loads in flight per thread
-    // (straight-line: a batch past the last survivor re-reads the last one
-    // and stores nothing).
+    // E == 1 (chunks of single elements, often short): the systematic
+    // survivors are copied as (element, survivor) items spread over the
+    // waves that do not eliminate, and the first CI items of each thread are
+    // loaded before the barrier that publishes the elimination's status (and
+    // stored only after it: a singular set writes nothing).
+    constexpr int CI = 4;
+    const int len = e1 - e0, items = len * first_par;
+    const int cw = m > 0 ? 1 : 0, nthr = kThreads - 64 * cw, ctid = tid - 64 * cw;
+    YT cy[CI];
+    int64_t co[CI];                      // output offset of item i, -1 for none
+    if constexpr (E == 1) {
+#pragma unroll
+        for (int i = 0; i < CI; ++i) {
+            const int it = ctid + i * nthr;
+            co[i] = -1;
+            cy[i] = YT(0);
+            if (ctid >= 0 && it < items) {
+                const int c = it / len, e = e0 + (it - c * len);
+                const int t = e / s, col = e - t * s;
+                const int w = sm.S[c];
+                if (t < sm.lim[w]) {
+                    cy[i] = Y[sm.yoff[c] + e];
+                    co[i] = sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col;
+                }
+            }
+        }
+    }
+
+    if (m > 0 && wv == 0) eliminate_set(a, sm, m, first_par, lane, sD);
+    __syncthreads();
+    if (sm.status != 0) {
+        if (writer) a.info[b] = sm.status;
+        return;
+    }
+    if (writer) a.info[b] = 0;
+
+    if constexpr (E == 1) {
+#pragma unroll
+        for (int i = 0; i < CI; ++i) {
+            if (co[i] >= 0) {
+                const float fv = static_cast<float>(cy[i]);   // the worker's result in the output type
+                store_out<1>(a, out, co[i], &fv);
+            }
+        }
+        for (int it = ctid + CI * nthr; ctid >= 0 && it < items; it += nthr) {
+            const int c = it / len, e = e0 + (it - c * len);
+            const int t = e / s, col = e - t * s;
+            const int w = sm.S[c];
+            if (t < sm.lim[w]) {
+                const float fv = static_cast<float>(Y[sm.yoff[c] + e]);
+                store_out<1>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, &fv);
+            }
+        }
+    }
+
+    // E == 4: U survivors' loads in flight per thread (straight-line: a batch
+    // past the last survivor re-reads the last one and stores nothing).
     constexpr int U = 8;
-    for (int e = e0 + E * tid; e < e1; e += E * kThreads) {
+    for (int e = e0 + E * tid; E == 4 && e < e1; e += E * kThreads) {
         const int t = e / s, col = e - t * s;
         const int64_t orow = static_cast<int64_t>(t) * a.ldo + col;
         for (int c0 = 0; c0 < first_par; c0 += U) {
