@@ -61,8 +61,41 @@ __global__ __launch_bounds__(kThreads) void shuffle_encode_kernel(const float* _
     if (m >= msgs) return;
     int64_t b, e;
     bool ok = term_range(off, m, terms, b, e) && e > b;
-    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q;
     float* dst = M + m * ldm;
+    if (ok && e - b <= 64) {
+        // lane j holds term j's row; one vote checks them all
+        const int cnt = static_cast<int>(e - b);
+        int32_t rj = 0;
+        bool bad = false;
+        if (lane < cnt) {
+            rj = rows[b + lane];
+            bad = rj < 0 || rj >= q;
+        }
+        ok = __ballot(bad) == 0;
+        for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
+            if (!ok) {
+                R::store(dst + c, R::nan());
+                continue;
+            }
+            auto row = [&](int j) __attribute__((always_inline)) {
+                return R::load(A + static_cast<int64_t>(__builtin_amdgcn_readlane(rj, j)) * lda + c);
+            };
+            typename R::T acc = row(0);
+            int j = 1;
+            for (; j + 4 <= cnt; j += 4) {
+                const typename R::T x0 = row(j), x1 = row(j + 1), x2 = row(j + 2), x3 = row(j + 3);
+                acc = acc + x0;
+                acc = acc + x1;
+                acc = acc + x2;
+                acc = acc + x3;
+            }
+            for (; j < cnt; ++j) acc = acc + row(j);
+            R::store(dst + c, acc);
+        }
+        return;
+    }
+    // more than 64 terms (no plan has them: n <= 64), or a bad range
+    for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q;
     for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
         if (!ok) {
             R::store(dst + c, R::nan());
@@ -104,9 +137,41 @@ __global__ __launch_bounds__(kThreads) void shuffle_decode_kernel(const float* _
     if (m >= msgs) return;
     int64_t b, e;
     if (!term_range(off, m, terms, b, e)) return;          // no term of this message can be placed
+    const int64_t cnt = e - b;
+    if (cnt <= kTermRegs) {
+        // lane j holds term j's row; one vote checks them all
+        int32_t rj = 0;
+        bool bad = false;
+        if (lane < cnt) {
+            rj = rows[b + lane];
+            bad = rj < 0 || rj >= q || msg[b + lane] != m;
+        }
+        const bool okv = __ballot(bad) == 0;
+        for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
+            if (!okv) {
+                for (int64_t d = b; d < e; ++d) R::store(out + d * ldo + c, R::nan());
+                continue;
+            }
+            const typename R::T mv = R::load(M + m * ldm + c);
+            typename R::T x[kTermRegs];
+#pragma unroll
+            for (int j = 0; j < kTermRegs; ++j)
+                if (j < cnt) x[j] = R::load(A + static_cast<int64_t>(__builtin_amdgcn_readlane(rj, j)) * lda + c);
+#pragma unroll
+            for (int i = 0; i < kTermRegs; ++i) {
+                if (i < cnt) {
+                    typename R::T acc = mv;
+#pragma unroll
+                    for (int j = 0; j < kTermRegs; ++j)
+                        if (j < cnt && j != i) acc = acc - x[j];
+                    R::store(out + (b + i) * ldo + c, acc);
+                }
+            }
+        }
+        return;
+    }
     bool ok = true;
     for (int64_t t = b; ok && t < e; ++t) ok = rows[t] >= 0 && rows[t] < q && msg[t] == m;
-    const int64_t cnt = e - b;
     for (int64_t c = static_cast<int64_t>(lane) * V; c < r; c += 64 * V) {
         if (!ok) {
             for (int64_t d = b; d < e; ++d) R::store(out + d * ldo + c, R::nan());
