@@ -166,3 +166,116 @@ def test_dense_bf16_workload_full_size(lib, torch):
         full_ref_scale = np.max(np.abs(ref), axis=0)
         err = float(np.max(np.max(np.abs(got - ref), axis=0) / full_ref_scale))
         assert err <= 2e-2, err
+
+
+def test_conditioned_gemv_workload_full_size(lib, torch):
+    """The certified (16,12) generator with one fp32 parity plane, A 65536 x 8192
+    fp32: coded_matmul for several draws with fresh x, as bench.py runs it."""
+    w = synth.WORKLOADS["gemv16x12_conditioned_65536x8192"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    P = synth.conditioned_parity_matrix(n, k, seed, w.extra["candidates"], pick=w.extra["parity_candidate"])[0]
+    code = lib.Code.systematic(P, w.extra["planes"])
+    assert code.planes == 1
+    dA = torch.from_numpy(A).cuda()
+    par = lib.alloc_parity(code, q, r, torch.float32)
+    ws = lib.alloc_y(code, q, 1, torch.float64)
+    out = torch.empty(q, dtype=torch.float32, device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    A64 = A.astype(np.float64)
+    for t in range(3):
+        x = synth.gaussian((r,), seed, synth.STREAM_X, t)
+        surv, _ = lib.coded_matmul(code, dA, par, torch.from_numpy(x).cuda(), out, ws, info, seed, t,
+                                   parity_ready=t > 0)
+        torch.cuda.synchronize()
+        S, _ = oc.draw_survivors(n, k, seed, t)
+        assert np.array_equal(surv, S) and int(info.item()) == 0
+        ref = oc.plain_product(A64, x)[:, 0]
+        err = float(np.max(np.abs(out.cpu().numpy() - ref)) / np.max(np.abs(ref)))
+        assert err <= TOL_F32, (t, err)
+
+
+def test_straggler_workload_full_size(lib, torch):
+    """Real straggling at the GEMV workload's size ((16,12), A 65536 x 8192 fp32),
+    survivors only, as bench.py runs it, coded and uncoded ((16,16) identity
+    code): each product against the oracle's fp64 A x, the survivors consistent
+    with the timeline, and the start times the runtime model's draws."""
+    from tests.test_gpu_straggler import check_timeline
+    w = synth.WORKLOADS["gemv16x12_65536x8192"]
+    n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
+    unit = 2000.0                                  # microseconds per unit of the runtime model
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    x = synth.gaussian((r,), seed, synth.STREAM_X, 0)
+    ref = oc.plain_product(A.astype(np.float64), x)[:, 0]
+    coded = lib.Code.systematic(synth.parity_matrix(n, k, seed), planes=2)
+    uncoded = lib.Code.systematic(np.zeros((0, n)), planes=2)
+    dA, dx = torch.from_numpy(A).cuda(), torch.from_numpy(x).cuda()
+    par = lib.alloc_parity(coded, q, r, torch.float32)
+    lib.coded_encode(coded, dA, par)
+    out = torch.empty(q, dtype=torch.float32, device="cuda")
+    info = torch.full((1,), 9, dtype=torch.int32, device="cuda")
+    for code, parity, kk in ((coded, par, k), (uncoded, None, n)):
+        Y = lib.alloc_y(code, q, 1, torch.float64)
+        for draw in range(2):
+            out.fill_(float("nan"))
+            surv, tl, lat = lib.coded_straggler_matmul(code, dA, parity, dx, Y, out, info, seed, draw, unit)
+            torch.cuda.synchronize()
+            assert int(info.item()) == 0
+            err = float(np.max(np.abs(out.cpu().numpy() - ref)) / np.max(np.abs(ref)))
+            assert err <= TOL_F32, (kk, draw, err)
+            check_timeline(n, kk, surv, tl, lat, False)
+            assert np.allclose(tl[:, 0], oc.worker_runtimes(n, kk, seed, draw) * unit, rtol=1e-12)
+
+
+def test_shuffle_workload_full_size(lib, torch):
+    """Coded shuffling at the size bench.py measures (n = 16 workers, 10^6 rows of
+    256 fp32, caches of 10^5 rows), two iterations.  The planner's tables equal
+    the oracle's plan; three runs of 1000 messages (first, middle, last) of the
+    coded rows, and the rows decoded from them, equal the oracle's encode and
+    decode bit for bit; and every decoded row is the row of A it stands for,
+    within the rounding of its message's fp32 sums (checked on the GPU)."""
+    from oracle import shuffle as sh
+    n, q, r, cache, seed = 16, 1_000_000, 256, 100_000, 8
+    A = synth.gaussian_rows(q, r, seed, synth.STREAM_A)
+    dA = torch.from_numpy(A).cuda()
+    st = lib.Shuffle(n, q, cache, seed)
+    ref = sh.initial_state(n, q, cache, seed)
+    for _ in range(2):
+        coded_rows, terms = st.plan()
+        tb = st.tables()
+        p = sh.plan(ref)
+        for key in ("enc_off", "enc_rows", "term_worker", "term_msg"):
+            assert np.array_equal(tb[key], getattr(p, key)), key
+        assert np.array_equal(tb["next_assign"], p.new_assign)
+        assert (coded_rows, terms) == (p.coded_rows, p.uncoded_rows)
+        dev = {key: torch.from_numpy(tb[key]).cuda() for key in ("enc_off", "enc_rows", "term_msg")}
+        M = torch.full((coded_rows, r), float("nan"), dtype=torch.float32, device="cuda")
+        out = torch.full((terms, r), float("nan"), dtype=torch.float32, device="cuda")
+        lib.coded_shuffle_encode(dA, dev["enc_off"], dev["enc_rows"], M)
+        lib.coded_shuffle_decode(dA, M, dev["enc_off"], dev["enc_rows"], dev["term_msg"], out)
+        torch.cuda.synchronize()
+        off = tb["enc_off"]
+        for m0 in (0, coded_rows // 2, coded_rows - 1000):
+            m1 = m0 + 1000
+            a, b = int(off[m0]), int(off[m1])
+            sub = sh.Plan(p.new_assign, [], off[m0:m1 + 1] - a, tb["enc_rows"][a:b], tb["term_worker"][a:b],
+                          tb["term_msg"][a:b] - m0, m1 - m0, b - a)
+            M_ref = sh.encode(A, sub)
+            assert np.array_equal(M[m0:m1].cpu().numpy(), M_ref), m0
+            assert np.array_equal(out[a:b].cpu().numpy(), sh.decode(A, M_ref, sub)), m0
+        # all rows: |decoded - A[row]| <= 2 c 2^-24 (sum of the message's |rows|), c its term count
+        rows = dev["enc_rows"].long()
+        msg = dev["term_msg"].long()
+        cnt = (dev["enc_off"][1:] - dev["enc_off"][:-1]).to(torch.float32)
+        absum = torch.zeros((coded_rows, r), dtype=torch.float32, device="cuda")
+        step = 100_000
+        for c0 in range(0, terms, step):
+            absum.index_add_(0, msg[c0:c0 + step], dA[rows[c0:c0 + step]].abs())
+        for c0 in range(0, terms, step):
+            mm = msg[c0:c0 + step]
+            err = (out[c0:c0 + step] - dA[rows[c0:c0 + step]]).abs()
+            bound = 2.0 * cnt[mm].unsqueeze(1) * 2.0 ** -24 * absum[mm]
+            assert bool((err <= bound).all()), c0
+        del M, out, absum
+        st.commit()
+        ref = sh.commit(ref, p)
