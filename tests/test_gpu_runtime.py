@@ -53,3 +53,25 @@ def test_simulation_argument_errors(lib, torch):
         lib.coded_simulate_runtimes(10, 4, 0, 0, t_repetition=t)     # 4 does not divide 10
     with pytest.raises(lib.CodedError):
         lib.coded_simulate_runtimes(10, 11, 0, 0, t_mds=t)
+
+
+def test_simulation_full_launch_sampled_draws(lib, torch):
+    """The launch bench.py times: (10,5), seed 6, 2^24 draws starting at draw
+    5 * 2^24.  Three windows of 2000 draws (start, middle, end) against the
+    oracle draw by draw, and every draw of the launch ordered as the model
+    requires (MDS <= 2-repetition, and all three at least the shift)."""
+    n, k, seed, draws = 10, 5, 6, 1 << 24
+    first = 5 * draws
+    out = [torch.full((draws,), float("nan"), dtype=torch.float64, device="cuda") for _ in range(3)]
+    lib.coded_simulate_runtimes(n, k, seed, first, *out)
+    torch.cuda.synchronize()
+    for off in (0, draws // 2 - 1000, draws - 2000):
+        ref = rt.simulate(n, k, seed, first + off, 2000, 1.0, 1.0)
+        for got, r in zip(out, ref):
+            g = got[off:off + 2000].cpu().numpy()
+            assert np.all(np.abs(g - r) <= 4 * np.finfo(np.float64).eps * np.abs(r)), off
+    tu, tr, tm = out
+    assert bool(torch.isfinite(tu).all().item() and torch.isfinite(tr).all().item() and torch.isfinite(tm).all().item())
+    assert bool((tm <= tr).all().item())
+    # every task time is shift plus a nonnegative exponential, scaled by the task's share
+    assert bool((tu >= 1.0 / n).all().item() and (tm >= 1.0 / k).all().item())
