@@ -93,3 +93,22 @@ def test_shuffle_bad_table_entries_give_nan_rows(lib, torch):
     in_bad = tb["term_msg"] == bad
     assert np.all(np.isnan(oh[in_bad]))
     assert np.array_equal(oh[~in_bad], sh.decode(A, M_ref, p)[~in_bad])
+
+
+def test_shuffle_nothing_to_send(lib, torch):
+    """Caches holding every row: the plan has no messages and no terms (as the
+    oracle's), both kernels accept the empty tables and enqueue nothing, and
+    the next iteration plans the same way."""
+    n, q, r = 4, 100, 64
+    A = synth.gaussian((q, r), 52, synth.STREAM_A)
+    dA = torch.from_numpy(A).cuda()
+    st = lib.Shuffle(n, q, q, 3)
+    ref = sh.initial_state(n, q, q, 3)
+    for _ in range(2):
+        tb, M, out = run_iteration(lib, torch, st, dA, r)
+        p = sh.plan(ref)
+        assert p.coded_rows == 0 and p.uncoded_rows == 0
+        assert M.shape == (0, r) and out.shape == (0, r)
+        assert np.array_equal(tb["enc_off"], p.enc_off) and np.array_equal(tb["next_assign"], p.new_assign)
+        st.commit()
+        ref = sh.commit(ref, p)
