@@ -287,6 +287,19 @@ def test_decode_errors(lib, torch):
         oc.decode(oc.systematic_generator(Pbad), [0, 1, 4, 5], [np.zeros((5, 1))] * 4, q)
 
 
+def test_decode_batched_zero_sets(lib, torch):
+    """An empty batch of survivor sets: nothing is enqueued, out and info untouched."""
+    n, k, q, r, s = 8, 6, 60, 32, 1
+    P, A, X = make_inputs(n, k, q, r, s, 61)
+    code = lib.Code.systematic(P, 2)
+    Y = lib.alloc_y(code, q, s, torch.float64)
+    sets = torch.zeros((0, k), dtype=torch.int32, device="cuda")
+    out = torch.zeros((0, q, s), dtype=torch.float32, device="cuda")
+    info = torch.zeros(0, dtype=torch.int32, device="cuda")
+    lib.coded_decode_batched(code, sets, Y, q, out, info)
+    torch.cuda.synchronize()
+
+
 def test_decode_batched_matches_single(lib, torch):
     n, k, q, s = 64, 48, 1000, 8
     P, A, X = make_inputs(n, k, q, 24, s, 12)

@@ -75,3 +75,10 @@ def test_simulation_full_launch_sampled_draws(lib, torch):
     assert bool((tm <= tr).all().item())
     # every task time is shift plus a nonnegative exponential, scaled by the task's share
     assert bool((tu >= 1.0 / n).all().item() and (tm >= 1.0 / k).all().item())
+
+
+def test_simulation_zero_draws(lib, torch):
+    """No draws: nothing is enqueued and the call succeeds."""
+    out = [torch.empty(0, dtype=torch.float64, device="cuda") for _ in range(3)]
+    lib.coded_simulate_runtimes(10, 5, 1, 0, *out)
+    torch.cuda.synchronize()
