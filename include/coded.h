@@ -217,7 +217,9 @@ coded_status coded_draw_survivors(int32_t n, int32_t k, uint64_t seed, uint64_t 
  * taken in order; a set is kept if it qualifies and differs from every set
  * kept before.  sets_out: host int32[batch*k], each row ascending.
  * next_draw_out (may be NULL): first draw not consumed.  Fails with
- * CODED_ERR_ARG if min_parity > min(k, n-k).
+ * CODED_ERR_ARG if min_parity > min(k, n-k), or if batch exceeds the number
+ * of distinct qualifying sets, sum over m >= min_parity of C(k,m) C(n-k,m)
+ * (checked before any draw, so the call always ends).
  */
 coded_status coded_draw_survivor_sets(int32_t n, int32_t k, uint64_t seed, uint64_t first_draw, int32_t batch,
                                       int32_t min_parity, int32_t* sets_out, uint64_t* next_draw_out);

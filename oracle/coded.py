@@ -156,7 +156,12 @@ def draw_survivor_sets(n: int, k: int, seed: int, batch: int, min_parity: int = 
     """`batch` distinct survivor sets with at least `min_parity` parity workers:
     draws first_draw, first_draw+1, ... are taken in order and a set is kept
     when it qualifies and differs from every set kept before.  Returns
-    (batch, k) int32 sets and the next unused draw index."""
+    (batch, k) int32 sets and the next unused draw index.  Asking for more
+    sets than exist (sum over m >= min_parity of C(k, m) C(n-k, m): m parity
+    workers in, m systematic ones out) raises ValueError."""
+    available = sum(math.comb(k, m) * math.comb(n - k, m) for m in range(min_parity, min(k, n - k) + 1))
+    if batch > available:
+        raise ValueError(f"only {available} distinct survivor sets have >= {min_parity} parity workers")
     seen = set()
     sets = []
     d = first_draw

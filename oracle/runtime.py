@@ -76,31 +76,36 @@ def cdf_mds(t, n: int, k: int, mu: float, shift: float = 1.0):
 
 
 def lambert_w_lower(x: float) -> float:
-    """W_{-1}(x) for -1/e <= x < 0: the solution w <= -1 of w e^w = x
-    (Halley's iteration on f(w) = w e^w - x)."""
+    """W_{-1}(x) for -1/e <= x < 0, from its definition: the solution w <= -1
+    of w e^w = x (Lemma 2 uses this lower real branch).
+
+    On (-inf, -1] the map f(w) = w e^w decreases monotonically from 0 (as
+    w -> -inf) to -1/e (at w = -1), so the root is unique.  It is bracketed
+    by [lo, -1] with lo pushed left until f(lo) > x, then found by plain
+    bisection: the bracket is halved until no fp64 value lies strictly
+    inside it, and the end whose f is nearer x is returned."""
     if not (-1.0 / math.e <= x < 0.0):
         raise ValueError("W_{-1} is real on [-1/e, 0)")
-    if x == -1.0 / math.e:
-        return -1.0
-    # start: near -1/e use the branch-point series in p = -sqrt(2 (1 + e x)),
-    # otherwise the asymptotic log form
-    if x < -0.25:
-        p = -math.sqrt(2.0 * (1.0 + math.e * x))
-        w = -1.0 + p - p * p / 3.0
-    else:
-        lx = math.log(-x)
-        w = lx - math.log(-lx)
-    for _ in range(100):
-        ew = math.exp(w)
-        f = w * ew - x
-        wp1 = w + 1.0
-        if wp1 == 0.0:
+
+    def f(w):
+        return w * math.exp(w)
+
+    hi = -1.0
+    if f(hi) >= x:                    # x at the branch point (within rounding)
+        return hi
+    lo = -2.0
+    while f(lo) <= x:                 # f(lo) must lie above x (nearer 0)
+        lo *= 2.0
+    # invariant: lo < hi, f(lo) > x >= f(hi)
+    while True:
+        mid = 0.5 * (lo + hi)
+        if not (lo < mid < hi):
             break
-        step = f / (ew * wp1 - (w + 2.0) * f / (2.0 * wp1))
-        w -= step
-        if abs(step) <= 1e-15 * abs(w):
-            break
-    return w
+        if f(mid) > x:
+            lo = mid
+        else:
+            hi = mid
+    return lo if abs(f(lo) - x) < abs(f(hi) - x) else hi
 
 
 def optimal_mds(n: int, mu: float):

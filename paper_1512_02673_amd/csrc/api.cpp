@@ -256,6 +256,28 @@ coded_status do_decode_single(const coded_code* c, const DecodeSet& set, int m, 
     return CODED_OK;
 }
 
+// Number of k-subsets of the n workers holding at least min_parity of the n-k
+// parity workers, saturating at 2^64 - 1 (binomials from Pascal's triangle in
+// saturating arithmetic; n <= CODED_MAX_N).
+uint64_t qualifying_sets(int n, int k, int min_parity) {
+    constexpr uint64_t kSat = ~0ull;
+    std::vector<std::vector<uint64_t>> C(n + 1, std::vector<uint64_t>(n + 1, 0));
+    for (int a = 0; a <= n; ++a) {
+        C[a][0] = 1;
+        for (int b = 1; b <= a; ++b) {
+            const uint64_t x = C[a - 1][b - 1], y = C[a - 1][b];
+            C[a][b] = x > kSat - y ? kSat : x + y;
+        }
+    }
+    uint64_t total = 0;
+    for (int m = min_parity; m <= std::min(k, n - k); ++m) {
+        const uint64_t x = C[k][m], y = C[n - k][m];
+        const uint64_t prod = (x != 0 && y > kSat / x) ? kSat : x * y;
+        total = prod > kSat - total ? kSat : total + prod;
+    }
+    return total;
+}
+
 }  // namespace
 }  // namespace coded
 
@@ -442,6 +464,11 @@ coded_status coded_draw_survivor_sets(int32_t n, int32_t k, uint64_t seed, uint6
     if (batch > 0 && !sets_out) return fail(CODED_ERR_ARG, "sets_out is NULL");
     if (min_parity < 0 || min_parity > std::min(k, n - k))
         return fail(CODED_ERR_ARG, "min_parity must lie in [0, min(k, n-k)]");
+    // Distinct sets with m >= min_parity parity members: sum_m C(k, m) C(n-k, m)
+    // (m parity workers in, m systematic ones out).  More are never found.
+    if (static_cast<uint64_t>(batch) > qualifying_sets(n, k, min_parity))
+        return fail(CODED_ERR_ARG, "batch exceeds the number of distinct survivor sets with at least min_parity "
+                                   "parity workers");
     std::set<std::vector<int32_t>> seen;
     std::vector<int32_t> cur(k);
     uint64_t d = first_draw;

@@ -50,6 +50,21 @@ def test_survivor_sets_match_oracle(lib):
     got, nxt = lib.coded_draw_survivor_sets(4, 2, 0, 6, min_parity=0)
     want, nxt_ref = oc.draw_survivor_sets(4, 2, 0, 6, min_parity=0)     # all C(4,2) sets
     assert np.array_equal(got, want) and nxt == nxt_ref
+    got, nxt = lib.coded_draw_survivor_sets(6, 3, 5, 10, min_parity=2)  # all 9 + 1 qualifying sets
+    want, nxt_ref = oc.draw_survivor_sets(6, 3, 5, 10, min_parity=2)
+    assert np.array_equal(got, want) and nxt == nxt_ref
+
+
+def test_survivor_set_batch_beyond_the_qualifying_sets_is_refused(lib):
+    """More sets than exist fail at once (no endless drawing): C(4,2) = 6 sets,
+    10 sets of (6,3) with at least 2 parity workers, 4 of (5,4) with its parity worker."""
+    for n, k, batch, m_min in [(4, 2, 7, 0), (6, 3, 11, 2), (5, 4, 5, 1)]:
+        with pytest.raises(lib.CodedError) as e:
+            lib.coded_draw_survivor_sets(n, k, 0, batch, min_parity=m_min)
+        assert e.value.status == lib.CODED_ERR_ARG
+    # one set with all 16 parity workers exists, and it is found
+    got, _ = lib.coded_draw_survivor_sets(20, 16, 0, 1, min_parity=4)
+    assert np.sum(got[0] >= 16) == 4
 
 
 def test_host_argument_errors(lib):

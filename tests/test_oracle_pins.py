@@ -302,6 +302,42 @@ def test_parity_survivor_count_is_hypergeometric(n, k):
     assert scipy.stats.chisquare(obs, exp).pvalue > 1e-3
 
 
+def test_accepted_survivor_sets_follow_the_conditioned_hypergeometric_law():
+    """The decode-heavy rule keeps sequential draws whose set has m >= 8 parity
+    workers and that differ from every kept set.  With C(64,48) ~ 4.9e14 sets,
+    repeats are negligible, so the kept sets' parity counts must follow the
+    law of the k fastest of n i.i.d. runtimes (Sec. III-B: every k-subset is
+    equally likely, m is hypergeometric) conditioned on m >= 8."""
+    n, k, m_min, B = 64, 48, 8, 4000
+    sets, _ = oc.draw_survivor_sets(n, k, 11, B, min_parity=m_min)
+    m = (sets >= k).sum(axis=1)
+    support = np.arange(m_min, n - k + 1)
+    w = np.array([math.comb(n - k, j) * math.comb(k, k - j) for j in support], dtype=np.float64)
+    probs = w / w.sum()
+    counts = np.array([np.sum(m == j) for j in support])
+    assert counts.sum() == B
+    keep = probs * B >= 5
+    obs, exp = counts[keep], probs[keep] * B
+    if np.any(~keep):
+        obs, exp = np.append(obs, counts[~keep].sum()), np.append(exp, probs[~keep].sum() * B)
+    assert scipy.stats.chisquare(obs, exp).pvalue > 1e-3
+
+
+def test_survivor_set_batch_limited_by_the_number_of_qualifying_sets():
+    """sum_{m >= m_min} C(k,m) C(n-k,m) sets exist; all of them come back when
+    that many are asked for, and one more is refused instead of drawing forever."""
+    n, k, m_min = 6, 3, 2
+    total = sum(math.comb(k, j) * math.comb(n - k, j) for j in range(m_min, min(k, n - k) + 1))
+    assert total == 10
+    sets, _ = oc.draw_survivor_sets(n, k, 5, total, min_parity=m_min)
+    every = {c for c in itertools.combinations(range(n), k) if sum(v >= k for v in c) >= m_min}
+    assert {tuple(int(v) for v in s) for s in sets} == every
+    with pytest.raises(ValueError):
+        oc.draw_survivor_sets(n, k, 5, total + 1, min_parity=m_min)
+    with pytest.raises(ValueError):
+        oc.draw_survivor_sets(4, 2, 0, 7)
+
+
 def test_survivor_sets_with_min_parity_are_distinct_and_qualify():
     n, k = 64, 48
     sets, nxt = oc.draw_survivor_sets(n, k, 4, 300, min_parity=8)

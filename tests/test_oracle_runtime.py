@@ -25,6 +25,33 @@ def test_lambert_w_lower_branch(x):
     assert abs(w * math.exp(w) - x) <= 1e-13
 
 
+@pytest.mark.parametrize("eps", [1e-12, 1e-9, 1e-6])
+def test_lambert_w_lower_near_the_branch_point(eps):
+    """Near x = -1/e the lower branch has the expansion
+    W_{-1}(-1/e + eps) = -1 - p - p^2/3 - 11 p^3/72 + O(p^4), p = sqrt(2 e eps)
+    (a closed form independent of both the bisection and scipy, which loses
+    accuracy here)."""
+    x = -math.exp(-1.0) + eps
+    p = math.sqrt(2.0 * math.e * eps)
+    series = -1.0 - p - p * p / 3.0 - 11.0 * p ** 3 / 72.0
+    w = rt.lambert_w_lower(x)
+    assert abs(w - series) <= 2.0 * p ** 4 + 1e-7
+
+
+def test_library_optimal_k_agrees_with_the_bisection_oracle():
+    """The library's k* and T* (its own W_{-1}) against the oracle's definition-based root."""
+    from paper_1512_02673_amd import binding as lib
+    try:
+        lib.lib()
+    except (OSError, RuntimeError) as e:
+        pytest.skip(f"library not built: {e}")
+    for n, mu in [(10, 1.0), (64, 0.25), (1000, 1.0), (100, 5.0), (7, 0.05)]:
+        ks, ts, kb = lib.coded_optimal_k(n, mu)
+        k_ref, t_ref, _ = rt.optimal_mds(n, mu)
+        assert ks == pytest.approx(k_ref, rel=1e-12) and ts == pytest.approx(t_ref, rel=1e-12)
+        assert kb == rt.best_integer_k(n, mu)
+
+
 def test_optimal_runtime_factor_printed_in_paper():
     g = json.load(open(os.path.join(GOLDEN, "optimal_mds_mu1.json")))
     _, _, nT = rt.optimal_mds(1000, g["mu"])
