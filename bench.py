@@ -436,11 +436,22 @@ def decode_workload(args):
     Y = lib.alloc_y(code, q, s, torch.float64)
     lib.coded_encode(code, dA, par)
     lib.coded_worker_mm(code, dA, par, dX, Y)
+    # The 64 worker products (s = 8 columns, fp64 matrix cores), timed on their own.
+    stream = torch.cuda.current_stream()
+    pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+    for e0, e1 in pev:
+        e0.record(stream)
+        lib.coded_worker_mm(code, dA, par, dX, Y)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    prod_ms = np.array([a.elapsed_time(b) for a, b in pev])
+    qb = code.qb(q)
+    prod_bytes = 4.0 * q * r + 4.0 * code.planes * (n - k) * qb * r + 4.0 * r * s + 8.0 * n * qb * s
+    prod_flops = 2.0 * (k * qb + code.planes * (n - k) * qb) * r * s
     sets, _ = lib.coded_draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
     dsets = torch.from_numpy(sets).cuda()
     out = torch.empty((B, q, s), dtype=torch.float32, device="cuda")
     info = torch.zeros(B, dtype=torch.int32, device="cuda")
-    stream = torch.cuda.current_stream()
     for _ in range(W):
         lib.coded_decode_batched(code, dsets, Y, q, out, info)
     torch.cuda.synchronize()
@@ -455,7 +466,6 @@ def decode_workload(args):
     if int(info.abs().sum().item()) != 0:
         raise RuntimeError("a decode reported a singular or invalid survivor set")
     ms = np.array([a.elapsed_time(b) for a, b in evs])
-    qb = code.qb(q)
     m = (sets >= k).sum(axis=1)
     algo_bytes = 4.0 * B * q * s + 8.0 * n * qb * s + 4.0 * B * k + 4.0 * B
     flops = float(np.sum(2.0 * m * k * qb * s))
@@ -471,6 +481,13 @@ def decode_workload(args):
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
                      "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
                      "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double>")},
+        "products": {"kernel": "gemm_f32_mfma_kernel<1, 2, true, 64, 4> (64 worker products, s = 8, once per run)",
+                     "ms_mean": float(prod_ms.mean()), "ms_min": float(prod_ms.min()),
+                     "algorithmic_bytes_per_launch": prod_bytes,
+                     "achieved_gbs": prod_bytes / (float(prod_ms.mean()) * 1e-3) / 1e9,
+                     "hbm_frac": prod_bytes / (float(prod_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "fp64_tflops": prod_flops / (float(prod_ms.mean()) * 1e-3) / 1e12,
+                     "traffic": measured_kernel_traffic(w.name, "gemm_f32_mfma_kernel<1, 2, true, 64, 4>", prod_bytes)},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)

@@ -61,6 +61,11 @@ struct WorkerArgs {
     uint8_t par_ids[kMaxN];
 };
 hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st);
+// fp32 with s > 1 on the fp64 matrix cores (worker_f32_mfma.hip); supported
+// when r and lda are multiples of 4, 0 < r <= 2^30 and A, parity are 16-byte
+// aligned.
+bool gemm_f32_mfma_supported(const WorkerArgs& a);
+hipError_t launch_gemm_f32_mfma(const WorkerArgs& a, hipStream_t st);
 hipError_t launch_worker_bf16(const WorkerArgs& a, hipStream_t st);
 // bf16: X (r x s, row stride ldx) transposed into a.xt.
 hipError_t launch_transpose_x_bf16(const WorkerArgs& a, hipStream_t st);

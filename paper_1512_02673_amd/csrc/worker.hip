@@ -11,7 +11,8 @@
 // that a whole workgroup issues over one contiguous stretch of a row at a time
 // (streaming each row through a single wavefront instead measurably loses
 // bandwidth).  Products of two fp32 values are exact in fp64 and are summed
-// in fp64.  s > 1 and unaligned shapes take a general kernel.
+// in fp64.  s > 1 runs on the fp64 matrix cores (worker_f32_mfma.hip);
+// unaligned shapes take a general vector kernel.
 #include "internal.h"
 #include "worker_common.h"
 
@@ -155,8 +156,9 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
 }
 
 // General shapes (any r, s, strides): one block row per wave (all planes of a
-// parity row), scalar loads, columns of X in groups of SC.  Used for s > 1
-// and for unaligned inputs.
+// parity row), scalar loads, columns of X in groups of SC.  Used for inputs
+// the vector GEMV and the matrix-core kernel cannot take (r or lda not a
+// multiple of 4, or unaligned pointers).
 template <int SC>
 __global__ __launch_bounds__(kThreads) void gemm_small_f32_kernel(WorkerArgs a) {
     int worker;
@@ -235,6 +237,7 @@ hipError_t launch_worker_f32(const WorkerArgs& a, hipStream_t st) {
         if (a.r > 1024) return launch_gemv_t<2>(a, st);
         return launch_gemv_t<1>(a, st);
     }
+    if (gemm_f32_mfma_supported(a)) return launch_gemm_f32_mfma(a, st);
     return launch_waves(gemm_small_f32_kernel<4>, a, a.qb, a.qb, st);
 }
 
