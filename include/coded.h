@@ -247,6 +247,31 @@ coded_status coded_matmul(const coded_code* code, coded_dtype dt, const void* A,
                           uint64_t draw, double shift, double rate, int32_t* survivors_out, double* t_overall_out,
                           float* out, int64_t ldo, void* workspace, int32_t* info, void* stream);
 
+/* Bytes of the device scratch that coded_matmul_noalloc uses on each GPU. */
+#define CODED_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * coded_matmul_noalloc -- coded_matmul for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments and results as coded_matmul, minus
+ * the workspace: the worker results (and, for bf16, X transposed) live in a
+ * library-owned static device array of CODED_NOALLOC_SCRATCH_BYTES bytes, one
+ * per GPU, held from the library's load until the process ends.  The call
+ * allocates and frees nothing.
+ *   A problem whose coded_sizes workspace_bytes exceeds
+ *   CODED_NOALLOC_SCRATCH_BYTES fails with CODED_ERR_UNSUPPORTED before
+ *   anything is enqueued.
+ *   Every call on a GPU uses that GPU's one array: calls that overlap on a
+ *   GPU (other threads, or other streams without ordering between them) race
+ *   on it; serialise them.  The array keeps the last call's worker results;
+ *   nothing in a call depends on its earlier contents.
+ */
+coded_status coded_matmul_noalloc(const coded_code* code, coded_dtype dt, const void* A, int64_t q, int64_t r,
+                                  int64_t lda, void* parity, int32_t parity_ready, const void* X, int64_t s,
+                                  int64_t ldx, uint64_t seed, uint64_t draw, double shift, double rate,
+                                  int32_t* survivors_out, double* t_overall_out, float* out, int64_t ldo,
+                                  int32_t* info, void* stream);
+
 /*
  * coded_straggler_matmul -- one coded product with real, timed straggling:
  * the master/worker protocol of Sec. III-A run against the clock, with the

@@ -19,6 +19,7 @@ CODED_OK, CODED_ERR_ARG, CODED_ERR_SHAPE, CODED_ERR_TOO_FEW, CODED_ERR_SINGULAR,
     CODED_ERR_UNSUPPORTED = range(7)
 CODED_F32, CODED_BF16, CODED_F64 = 0, 1, 2
 CODED_MAX_N = 128
+CODED_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "coded.h")
 
@@ -41,6 +42,8 @@ _SIGNATURES = {
     "coded_draw_survivor_sets": (_c_i32, [_c_i32, _c_i32, _c_u64, _c_u64, _c_i32, _c_i32, _c_p, _c_p]),
     "coded_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i32, _c_p, _c_i64, _c_i64,
                               _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p, _c_p]),
+    "coded_matmul_noalloc": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_i32, _c_p, _c_i64, _c_i64,
+                                      _c_u64, _c_u64, _c_dbl, _c_dbl, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]),
     "coded_straggler_matmul": (_c_i32, [_c_p, _c_i32, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i64,
                                         _c_u64, _c_u64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_p, _c_i32, _c_p, _c_p,
                                         _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
@@ -303,6 +306,24 @@ def coded_matmul(code: Code, A, parity, X, out, workspace, info, seed: int, draw
     _check(lib().coded_matmul(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity), int(bool(parity_ready)),
                               _ptr(X), s, ldx, seed, draw, shift, rate, surv.ctypes.data_as(ctypes.c_void_p),
                               ctypes.addressof(t), _ptr(out), ldo, _ptr(workspace), _ptr(info), _stream(stream)))
+    return surv, t.value
+
+
+def coded_matmul_noalloc(code: Code, A, parity, X, out, info, seed: int, draw: int, parity_ready: bool = True,
+                         shift: float = 1.0, rate: float = 1.0, stream=None):
+    """coded_matmul on the library's static device scratch (no workspace argument,
+    nothing allocated); returns (survivors int32[k], T_(k))."""
+    q, r, lda = _matrix(A, "A")
+    rx, s, ldx = _matrix(X, "X")
+    if rx != r:
+        raise ValueError("X must have r rows")
+    _, so, ldo = _matrix(out, "out")
+    surv = np.zeros(code.k, dtype=np.int32)
+    t = ctypes.c_double()
+    _check(lib().coded_matmul_noalloc(code.handle, _dtype_code(A), _ptr(A), q, r, lda, _ptr(parity),
+                                      int(bool(parity_ready)), _ptr(X), s, ldx, seed, draw, shift, rate,
+                                      surv.ctypes.data_as(ctypes.c_void_p), ctypes.addressof(t), _ptr(out), ldo,
+                                      _ptr(info), _stream(stream)))
     return surv, t.value
 
 

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "survivors.cpp", "shuffle.cpp", "encode.hip", "worker.hip", "worker_f32_mfma.hip", "worker_bf16.hip", "fused_bf16.hip",
-           "decode.hip", "onepass.hip", "transpose.hip", "runtime.hip", "shuffle.hip"]
+           "decode.hip", "onepass.hip", "transpose.hip", "runtime.hip", "shuffle.hip", "scratch.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result", f"-I{os.path.join(ROOT, 'include')}"]
 # Device code: gfx950 only; packed-fp32 instructions disabled.

@@ -559,6 +559,28 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     CODED_GUARD_END
 }
 
+coded_status coded_matmul_noalloc(const coded_code* c, coded_dtype dt, const void* A, int64_t q, int64_t r,
+                                  int64_t lda, void* parity, int32_t parity_ready, const void* X, int64_t s,
+                                  int64_t ldx, uint64_t seed, uint64_t draw, double shift, double rate,
+                                  int32_t* survivors_out, double* t_overall_out, float* out, int64_t ldo,
+                                  int32_t* info, void* stream) {
+    CODED_GUARD_BEGIN
+    if (coded_status st = check_code(c)) return st;
+    const coded_dtype y_dt = dt == CODED_F32 ? CODED_F64 : CODED_F32;
+    if (coded_status st = check_dt(dt, y_dt)) return st;
+    if (q < 0 || r < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q, r, s must be >= 0");
+    const int64_t need = matmul_y_bytes(c, dt, q, s) + (dt == CODED_BF16 ? worker_workspace_bytes_bf16(r, s) : 0);
+    if (need > static_cast<int64_t>(CODED_NOALLOC_SCRATCH_BYTES))
+        return fail(CODED_ERR_UNSUPPORTED, "the product needs " + std::to_string(need) +
+                                               " bytes of workspace; the static scratch holds " +
+                                               std::to_string(static_cast<int64_t>(CODED_NOALLOC_SCRATCH_BYTES)));
+    void* ws = nullptr;
+    if (coded_status st = static_scratch(&ws)) return st;
+    return coded_matmul(c, dt, A, q, r, lda, parity, parity_ready, X, s, ldx, seed, draw, shift, rate, survivors_out,
+                        t_overall_out, out, ldo, ws, info, stream);
+    CODED_GUARD_END
+}
+
 namespace {
 
 constexpr int kStragglerStreams = 4;          // the device's default number of hardware queues

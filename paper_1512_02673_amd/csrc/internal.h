@@ -122,6 +122,11 @@ hipError_t launch_shuffle_decode(const float* A, int64_t q, int64_t r, int64_t l
                                  const int64_t* off, const int32_t* rows, const int32_t* msg, int64_t msgs,
                                  int64_t terms, float* out, int64_t ldo, hipStream_t st);
 
+// ---------------------------------------------------------------- static scratch
+// Device address of the library's static scratch array on the current device
+// (CODED_NOALLOC_SCRATCH_BYTES bytes, looked up once per device).
+coded_status static_scratch(void** out);
+
 // ---------------------------------------------------------------- runtime model
 hipError_t launch_runtime_sim(int n, int k, uint64_t seed, uint64_t first, int64_t count, double shift, double rate,
                               double* t_uncoded, double* t_repetition, double* t_mds, hipStream_t st);

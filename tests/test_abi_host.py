@@ -140,3 +140,12 @@ def test_shuffle_argument_errors(lib):
         st.commit()                                          # nothing planned
     assert h.coded_shuffle_tables(st.handle, None, None, None, None, None) == lib.CODED_ERR_ARG
     assert h.coded_shuffle_plan(None, None, None) == lib.CODED_ERR_ARG
+
+
+def test_noalloc_scratch_size_matches_header(lib):
+    """The binding's copy of CODED_NOALLOC_SCRATCH_BYTES equals the header's definition."""
+    import re
+    text = open(lib.HEADER).read()
+    m = re.search(r"#define\s+CODED_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", text)
+    assert m, "CODED_NOALLOC_SCRATCH_BYTES not found in the header"
+    assert lib.CODED_NOALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
