@@ -37,8 +37,9 @@
  *    before anything is enqueued; they return a status and set a
  *    thread-local message (coded_last_error).  Numerical singularity of a
  *    survivor set is found on the device and reported through `info`.
- *  - The caller owns every buffer.  Apart from the code object made by
- *    coded_code_create, the library allocates no device memory.
+ *  - The caller owns every device buffer, the code's device copy of G
+ *    included (coded_code_bytes gives its size); the library allocates and
+ *    frees no device memory.
  *  - Nothing throws across this interface.
  */
 #ifndef CODED_H
@@ -73,6 +74,13 @@ typedef enum coded_dtype {
 typedef struct coded_code coded_code;
 
 /*
+ * coded_code_bytes -- bytes of the caller-owned device buffer a code needs:
+ * G (n*k doubles) and, when n > k, the parity rows P ((n-k)*k floats) for
+ * the matrix-core encode, each starting 256-byte aligned.
+ */
+coded_status coded_code_bytes(int32_t n, int32_t k, int64_t* bytes);
+
+/*
  * coded_code_create -- make the code used by every other call (Sec. III-A:
  * the (n,k) MDS code applied to the k sub-matrices).
  *   n, k      1 <= k <= n <= CODED_MAX_N.
@@ -82,12 +90,19 @@ typedef struct coded_code coded_code;
  *             invertible); a set that is not invertible is reported at
  *             decode time through info.
  *   planes    parity storage planes: 2 (hi + lo, default recipe) or 1.
- *   out       receives the new code.  The call copies G to the current
- *             device (one small allocation, synchronous); destroy with
- *             coded_code_destroy.  Device work that uses the code must be
- *             finished before destroying it.
+ *   device_buf, device_buf_bytes
+ *             caller-owned device memory of the current device, 16-byte
+ *             aligned, at least coded_code_bytes(n, k) bytes (else
+ *             CODED_ERR_ARG).  The call copies G (and P) into it
+ *             synchronously; the kernels read it, so it must stay allocated
+ *             and unmodified until the code is destroyed.
+ *   out       receives the new code (a host object: the host copy of G, and
+ *             the straggler runner's streams and events once used); destroy
+ *             with coded_code_destroy.  Device work that uses the code must
+ *             be finished before destroying it or freeing device_buf.
  */
-coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, coded_code** out);
+coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, void* device_buf,
+                               int64_t device_buf_bytes, coded_code** out);
 coded_status coded_code_destroy(coded_code* code);
 coded_status coded_code_info(const coded_code* code, int32_t* n, int32_t* k, int32_t* planes);
 

@@ -26,7 +26,8 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 _c_i32, _c_i64, _c_u64, _c_dbl, _c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p
 
 _SIGNATURES = {
-    "coded_code_create": (_c_i32, [_c_i32, _c_i32, _c_p, _c_i32, ctypes.POINTER(_c_p)]),
+    "coded_code_bytes": (_c_i32, [_c_i32, _c_i32, _c_p]),
+    "coded_code_create": (_c_i32, [_c_i32, _c_i32, _c_p, _c_i32, _c_p, _c_i64, ctypes.POINTER(_c_p)]),
     "coded_code_destroy": (_c_i32, [_c_p]),
     "coded_code_info": (_c_i32, [_c_p, _c_p, _c_p, _c_p]),
     "coded_sizes": (_c_i32, [_c_p, _c_i32, _c_i32, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]),
@@ -176,15 +177,27 @@ def _matrix(t, name):
     return t.shape[0], t.shape[1], max(t.stride(0), 1)
 
 
+def coded_code_bytes(n: int, k: int) -> int:
+    """Bytes of the device buffer an (n,k) code needs."""
+    b = ctypes.c_int64()
+    _check(lib().coded_code_bytes(n, k, ctypes.addressof(b)))
+    return b.value
+
+
 class Code:
-    """An (n,k) code: G = [I_k; P] on host and device (coded_code_create)."""
+    """An (n,k) code: G = [I_k; P] on host, and on the device in a buffer this
+    object owns (a torch tensor on the current device) and passes to
+    coded_code_create."""
 
     def __init__(self, n: int, k: int, G: np.ndarray, planes: int = 2):
         G = np.ascontiguousarray(G, dtype=np.float64)
         if G.shape != (n, k):
             raise ValueError("G must be n x k")
+        nbytes = coded_code_bytes(n, k)
+        self.device_buf = _torch().empty(nbytes, dtype=_torch().uint8, device="cuda")
         h = ctypes.c_void_p()
-        _check(lib().coded_code_create(n, k, G.ctypes.data, planes, ctypes.byref(h)))
+        _check(lib().coded_code_create(n, k, G.ctypes.data, planes, ctypes.c_void_p(self.device_buf.data_ptr()),
+                                       nbytes, ctypes.byref(h)))
         self.handle = h
         self.n, self.k, self.planes = n, k, planes
         self.G = G

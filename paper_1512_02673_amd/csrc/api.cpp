@@ -55,6 +55,13 @@ coded_status check_code(const coded_code* c) {
 
 int64_t block_rows(int64_t q, int k) { return (q + k - 1) / k; }
 
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+// The code's device buffer: G (n*k doubles), then P ((n-k)*k floats), each 256-byte aligned.
+int64_t code_device_bytes(int n, int k) {
+    return align256(static_cast<int64_t>(n) * k * 8) + (n > k ? align256(static_cast<int64_t>(n - k) * k * 4) : 0);
+}
+
 // coded_matmul's workspace: its worker results Y (fp64 for fp32 inputs, fp32
 // for bf16), 256-byte aligned, then the worker workspace.
 int64_t matmul_y_bytes(const coded_code* c, coded_dtype dt, int64_t q, int64_t s) {
@@ -285,7 +292,17 @@ using namespace coded;
 
 extern "C" {
 
-coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, coded_code** out) {
+coded_status coded_code_bytes(int32_t n, int32_t k, int64_t* bytes) {
+    CODED_GUARD_BEGIN
+    if (!bytes) return fail(CODED_ERR_ARG, "bytes is NULL");
+    if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
+    *bytes = code_device_bytes(n, k);
+    return CODED_OK;
+    CODED_GUARD_END
+}
+
+coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t planes, void* device_buf,
+                               int64_t device_buf_bytes, coded_code** out) {
     CODED_GUARD_BEGIN
     if (!out) return fail(CODED_ERR_ARG, "out is NULL");
     *out = nullptr;
@@ -298,24 +315,37 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
         for (int j = 0; j < k; ++j)
             if (G[i * k + j] != (i == j ? 1.0 : 0.0))
                 return fail(CODED_ERR_UNSUPPORTED, "only systematic codes (rows 0..k-1 of G equal to I_k) are supported");
+    const int64_t need = code_device_bytes(n, k);
+    if (!device_buf) return fail(CODED_ERR_ARG, "device_buf is NULL");
+    if (device_buf_bytes < need)
+        return fail(CODED_ERR_ARG, "device_buf holds " + std::to_string(device_buf_bytes) + " bytes; the code needs " +
+                                       std::to_string(need));
+    if (!aligned16(device_buf)) return fail(CODED_ERR_ARG, "device_buf must be 16-byte aligned");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    hipPointerAttribute_t attr{};
+    e = hipPointerGetAttributes(&attr, device_buf);
+    if (e != hipSuccess || attr.type != hipMemoryTypeDevice || attr.device != dev) {
+        (void)hipGetLastError();
+        return fail(CODED_ERR_ARG, "device_buf must be device memory of the current device");
+    }
     auto* c = new coded_code();
     c->n = n;
     c->k = k;
     c->planes = planes;
+    c->device = dev;
     c->G.assign(G, G + static_cast<size_t>(n) * k);
-    hipError_t e = hipGetDevice(&c->device);
-    if (e == hipSuccess) e = hipMalloc(&c->dG, c->G.size() * sizeof(double));
-    if (e == hipSuccess) e = hipMemcpy(c->dG, c->G.data(), c->G.size() * sizeof(double), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&c->compute_units, hipDeviceAttributeMultiprocessorCount, c->device);
+    c->dG = static_cast<double*>(device_buf);
+    e = hipMemcpy(c->dG, c->G.data(), c->G.size() * sizeof(double), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&c->compute_units, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess && n > k) {
         std::vector<float> pf(static_cast<size_t>(n - k) * k);
         for (size_t i = 0; i < pf.size(); ++i) pf[i] = static_cast<float>(c->G[static_cast<size_t>(k) * k + i]);
-        e = hipMalloc(&c->dPf, pf.size() * sizeof(float));
-        if (e == hipSuccess) e = hipMemcpy(c->dPf, pf.data(), pf.size() * sizeof(float), hipMemcpyHostToDevice);
+        c->dPf = reinterpret_cast<float*>(static_cast<char*>(device_buf) + align256(static_cast<int64_t>(n) * k * 8));
+        e = hipMemcpy(c->dPf, pf.data(), pf.size() * sizeof(float), hipMemcpyHostToDevice);
     }
     if (e != hipSuccess) {
-        if (c->dPf) (void)hipFree(c->dPf);
-        if (c->dG) (void)hipFree(c->dG);
         delete c;
         return hip_fail(e, "coded_code_create");
     }
@@ -327,17 +357,10 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
 coded_status coded_code_destroy(coded_code* c) {
     CODED_GUARD_BEGIN
     if (!c) return CODED_OK;
-    hipError_t e = hipSuccess;
     for (hipEvent_t ev : c->worker_events) hipEventDestroy(ev);
     if (c->start_event) hipEventDestroy(c->start_event);
     for (hipStream_t w : c->worker_streams) hipStreamDestroy(w);
-    if (c->dG) e = hipFree(c->dG);
-    if (c->dPf) {
-        const hipError_t e2 = hipFree(c->dPf);
-        if (e == hipSuccess) e = e2;
-    }
     delete c;
-    if (e != hipSuccess) return hip_fail(e, "coded_code_destroy");
     return CODED_OK;
     CODED_GUARD_END
 }
@@ -770,10 +793,6 @@ coded_status coded_transpose(const float* A, int64_t q, int64_t r, int64_t lda, 
     return CODED_OK;
     CODED_GUARD_END
 }
-
-namespace {
-int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
-}  // namespace
 
 coded_status coded_gd_sizes(const coded_code* cA, const coded_code* cT, int64_t q, int64_t r,
                             int64_t* workspace_bytes) {

@@ -12,8 +12,8 @@
 struct coded_code {
     int32_t n = 0, k = 0, planes = 2;
     std::vector<double> G;     // host copy, n*k row-major
-    double* dG = nullptr;      // device copy, n*k row-major
-    float* dPf = nullptr;      // device copy of the parity rows P ((n-k) x k) in fp32
+    double* dG = nullptr;      // device copy, n*k row-major (in the caller's buffer)
+    float* dPf = nullptr;      // device copy of the parity rows P ((n-k) x k) in fp32 (same buffer)
     int device = 0;
     int compute_units = 0;     // of the device, for kernels that place one workgroup per unit
     // Created on first use by coded_straggler_matmul, released with the code:

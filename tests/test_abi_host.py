@@ -80,12 +80,12 @@ def test_host_argument_errors(lib):
     h = lib.lib()
     # NULL pointers are rejected, not dereferenced
     assert h.coded_draw_survivors(4, 2, 0, 0, 1.0, 1.0, None, None) == lib.CODED_ERR_ARG
-    assert h.coded_code_create(4, 2, None, 2, ctypes.byref(ctypes.c_void_p())) == lib.CODED_ERR_ARG
+    assert h.coded_code_create(4, 2, None, 2, None, 0, ctypes.byref(ctypes.c_void_p())) == lib.CODED_ERR_ARG
     G = np.vstack([np.eye(2), np.ones((2, 2))])
     G[0, 1] = 0.5                                               # not systematic
-    assert h.coded_code_create(4, 2, G.ctypes.data, 2, ctypes.byref(ctypes.c_void_p())) == \
+    assert h.coded_code_create(4, 2, G.ctypes.data, 2, None, 0, ctypes.byref(ctypes.c_void_p())) == \
         lib.CODED_ERR_UNSUPPORTED
-    assert h.coded_code_create(4, 2, np.eye(4, 2).ctypes.data, 3, ctypes.byref(ctypes.c_void_p())) == \
+    assert h.coded_code_create(4, 2, np.eye(4, 2).ctypes.data, 3, None, 0, ctypes.byref(ctypes.c_void_p())) == \
         lib.CODED_ERR_ARG
     assert h.coded_encode(None, 0, None, 0, 0, 1, None, None) == lib.CODED_ERR_ARG
     assert h.coded_encode_worker_mm(None, 1, None, 0, 0, 1, None, None, 0, 1, None, 0, None, None) == \
@@ -149,3 +149,21 @@ def test_noalloc_scratch_size_matches_header(lib):
     m = re.search(r"#define\s+CODED_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", text)
     assert m, "CODED_NOALLOC_SCRATCH_BYTES not found in the header"
     assert lib.CODED_NOALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
+
+
+def test_code_device_buffer_is_the_callers(lib):
+    """coded_code_bytes sizes the caller's buffer (G in fp64, then P in fp32, each
+    256-byte aligned); coded_code_create refuses a missing or short buffer before
+    touching the device."""
+    assert lib.coded_code_bytes(4, 2) == 256 + 256
+    assert lib.coded_code_bytes(4, 4) == 256
+    assert lib.coded_code_bytes(64, 48) == 64 * 48 * 8 + 16 * 48 * 4
+    assert lib.coded_code_bytes(20, 16) == 2560 + 256
+    assert lib.coded_code_bytes(5, 3) == 256 + 256                 # 120 B of G, 24 B of P
+    h = lib.lib()
+    G = np.vstack([np.eye(2), np.ones((2, 2))])
+    out = ctypes.c_void_p()
+    assert h.coded_code_create(4, 2, G.ctypes.data, 2, None, 512, ctypes.byref(out)) == lib.CODED_ERR_ARG
+    assert "device_buf" in lib.last_error()
+    with pytest.raises(lib.CodedError):
+        lib.coded_code_bytes(2, 3)
