@@ -138,34 +138,43 @@ def test_gd_workload_full_size(lib, torch):
 
 
 def test_dense_bf16_workload_full_size(lib, torch):
-    """(32,24) code, A 131072 x 16384 bf16, X 16384 x 64 bf16, fp32 accumulation: two full calls
-    (encode + matrix-core worker products + decode); sampled block rows of every block against
-    the oracle's fp64 product (max normwise error 2e-2), survivors against the oracle."""
+    """(32,24) code, A 131072 x 16384 bf16, X 16384 x 64 bf16, fp32 accumulation: the first five
+    calls as bench.py makes them (encode + matrix-core worker products + decode, fresh X and draw
+    each); every output row of every call against the oracle's fp64 product (normwise per column,
+    2e-2), survivors against the oracle's draw."""
     w = synth.WORKLOADS["gemm_bf16_32x24_131072x16384x64"]
     n, k, q, r, s, seed = w.n, w.k, w.q, w.r, w.s, w.seed
+    calls = 5
     A = synth.bf16_round(synth.gaussian_rows(q, r, seed, synth.STREAM_A))
     P = synth.parity_matrix(n, k, seed, dtype="bf16")
     code = lib.Code.systematic(P, 2)
     dA = torch.from_numpy(synth.bf16_bits(A).view(np.int16)).cuda().view(torch.bfloat16)
     par = lib.alloc_parity(code, q, r, torch.bfloat16)
-    out = torch.empty((q, s), dtype=torch.float32, device="cuda")
-    info = torch.zeros(1, dtype=torch.int32, device="cuda")
-    qb = code.qb(q)
-    rng = np.random.default_rng(0)
-    for t in range(2):
+    outs = torch.empty((calls, q, s), dtype=torch.float32, device="cuda")
+    info = torch.full((calls,), -7, dtype=torch.int32, device="cuda")
+    Xs = []
+    for t in range(calls):
         X = synth.bf16_round(synth.gaussian((r, s), seed, synth.STREAM_X, t))
+        Xs.append(X)
         dX = torch.from_numpy(synth.bf16_bits(X).view(np.int16)).cuda().view(torch.bfloat16)
         ws = lib.matmul_workspace(code, dA, dX)
-        surv, _ = lib.coded_matmul(code, dA, par, dX, out, ws, info, seed, t, parity_ready=False)
-        torch.cuda.synchronize()
-        assert np.array_equal(surv, oc.draw_survivors(n, k, seed, t)[0]) and int(info.item()) == 0
-        ts = rng.choice(qb, size=24, replace=False)
-        rows = np.array([j * qb + tt for j in range(k) for tt in ts if j * qb + tt < q])
-        ref = oc.plain_product(A[rows], X)
-        got = out.cpu().numpy()[rows].astype(np.float64)
-        full_ref_scale = np.max(np.abs(ref), axis=0)
-        err = float(np.max(np.max(np.abs(got - ref), axis=0) / full_ref_scale))
-        assert err <= 2e-2, err
+        surv, _ = lib.coded_matmul(code, dA, par, dX, outs[t], ws, info[t:t + 1], seed, t, parity_ready=False)
+        assert np.array_equal(surv, oc.draw_survivors(n, k, seed, t)[0])
+    torch.cuda.synchronize()
+    assert np.all(info.cpu().numpy() == 0)
+    del dA, par
+    got = outs.cpu().numpy()                                   # (calls, q, s)
+    Xall = np.concatenate(Xs, axis=1)                          # (r, calls * s): one fp64 product per row block
+    max_diff = np.zeros(calls * s)
+    max_ref = np.zeros(calls * s)
+    for r0 in range(0, q, 4096):
+        ref = oc.plain_product(A[r0:r0 + 4096], Xall)          # fp64
+        g = got[:, r0:r0 + 4096, :].transpose(1, 0, 2).reshape(ref.shape[0], calls * s)
+        max_diff = np.maximum(max_diff, np.max(np.abs(g - ref), axis=0))
+        max_ref = np.maximum(max_ref, np.max(np.abs(ref), axis=0))
+    err = float(np.max(max_diff / max_ref))
+    print(f"dense full size: {calls} calls x {q} rows x {s} columns, max normwise error {err:.3e}")
+    assert err <= 2e-2, err
 
 
 def test_conditioned_gemv_workload_full_size(lib, torch):
