@@ -547,14 +547,15 @@ def gd_workload(args):
 
     from paper_1512_02673_amd import binding as lib
 
-    w = synth.WORKLOADS["gd20x16_262144x4096"]
+    w = synth.WORKLOADS[args.workload if args.workload.startswith("gd20x16") else "gd20x16_262144x4096"]
     n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
     K, W = args.steps, args.warmup
     A = synth.gaussian_rows(q, r, seed, synth.STREAM_A, std=w.a_std)
     wstar = synth.gaussian((r,), seed, synth.STREAM_WSTAR)
     noise = synth.gaussian((q,), seed, synth.STREAM_NOISE)
-    cA = lib.Code.systematic(synth.parity_matrix(n, k, seed), 2)
-    cT = lib.Code.systematic(synth.parity_matrix(n, k, seed, synth.STREAM_PT), 2)
+    PA, PT, planes = synth.gd_codes(w)
+    cA = lib.Code.systematic(PA, planes)
+    cT = lib.Code.systematic(PT, planes)
     dA = torch.from_numpy(A).cuda()
     # y = A w* + noise, formed once on the device in fp64 as input preparation
     dy = (dA.double() @ torch.from_numpy(wstar).cuda().double() +
@@ -597,15 +598,18 @@ def gd_workload(args):
     tA = float(np.mean([g[2 * i][0].elapsed_time(g[2 * i][1]) for i in range(20)]))
     tT = float(np.mean([g[2 * i + 1][0].elapsed_time(g[2 * i + 1][1]) for i in range(20)]))
     qbA, qbT = cA.qb(q), cT.qb(r)
-    bA = 4.0 * q * r + 4.0 * 2 * (n - k) * qbA * r + 4.0 * r + 8.0 * n * qbA
-    bT = 4.0 * r * q + 4.0 * 2 * (n - k) * qbT * q + 4.0 * q + 8.0 * n * qbT
+    bA = 4.0 * q * r + 4.0 * planes * (n - k) * qbA * r + 4.0 * r + 8.0 * n * qbA
+    bT = 4.0 * r * q + 4.0 * planes * (n - k) * qbT * q + 4.0 * q + 8.0 * n * qbT
     achieved = (bA + bT) / ((tA + tT) * 1e-3) / 1e9
     result = {
         "metric": METRIC, "value": K / elapsed, "unit": "iterations/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64", "data": "synthetic",
         "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "eta_applied": eta,
-                   "codes": "separate (20,16) systematic codes for A and A^T, hi+lo parity"},
+                   "codes": ("separate (20,16) systematic codes for A and A^T, hi+lo parity" if planes == 2 else
+                             "separate certified (20,16) codes for A and A^T (worst decode condition "
+                             f"{w.extra['worst_condition']} and {w.extra['worst_condition_T']}), one fp32 parity plane"),
+                   "parity_planes": planes},
         "gemv_A_ms": tA, "gemv_AT_ms": tT,
         "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel (A and A^T launches)", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
@@ -991,7 +995,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
                     choices=["gemv16x12_65536x8192", "gemv16x12_conditioned_65536x8192", "mds4x2_2048x512",
-                             "decode64x48_16384x4096x8", "gd20x16_262144x4096",
+                             "decode64x48_16384x4096x8", "gd20x16_262144x4096", "gd20x16_conditioned_262144x4096",
                              "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
                              "straggler16x12_65536x8192", "shuffle16_1000000x256"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -1047,7 +1051,7 @@ def main():
         if "--warmup" not in sys.argv:
             args.warmup = 3
         result = straggler_workload(args)
-    elif args.workload == "gd20x16_262144x4096":
+    elif args.workload.startswith("gd20x16"):
         if "--steps" not in sys.argv:
             args.steps = 200
         if "--warmup" not in sys.argv:

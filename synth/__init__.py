@@ -11,4 +11,4 @@ from .inputs import (  # noqa: F401
     bf16_round, bf16_bits, bf16_from_bits, parity_matrix, integer_parity_matrix,
     worst_decode_condition, conditioned_parity_matrix,
 )
-from .workloads import WORKLOADS, Workload  # noqa: F401
+from .workloads import WORKLOADS, Workload, gd_codes  # noqa: F401

@@ -47,4 +47,30 @@ WORKLOADS = {
     "gd20x16_262144x4096": Workload("gd20x16_262144x4096", 20, 16, 262144, 4096, 1, "f32", 5, 200,
                                     a_std=1.0 / 64.0,
                                     extra={"eta": 0.5, "noise_std": 0.1}),
+    # Coded gradient descent with certified generators and one fp32 parity
+    # plane: of 20000 seeded N(0,1) parity matrices per code
+    # (synth.conditioned_parity_matrix(20, 16, 5, 20000, stream)), candidate
+    # 19453 (code of A, stream P) and 2856 (code of A^T, stream P_T) have the
+    # smallest worst decode condition numbers, 1656.6 and 1634.3 over every
+    # survivor set (the plain draws: 102128 and 3518).
+    "gd20x16_conditioned_262144x4096": Workload("gd20x16_conditioned_262144x4096", 20, 16, 262144, 4096, 1, "f32",
+                                                5, 200, a_std=1.0 / 64.0,
+                                                extra={"eta": 0.5, "noise_std": 0.1, "planes": 1,
+                                                       "candidates": 20000, "parity_candidate": 19453,
+                                                       "parity_candidate_T": 2856, "worst_condition": 1656.6,
+                                                       "worst_condition_T": 1634.3}),
 }
+
+
+def gd_codes(w: Workload):
+    """Parity matrices of the two codes of a coded gradient-descent workload (the
+    code of A from stream P, the code of A^T from stream P_T) and the parity
+    planes they are stored with: the plain seeded draws with two planes, or
+    the workload's certified candidates with its plane count."""
+    from .inputs import STREAM_P, STREAM_PT, conditioned_parity_matrix, parity_matrix
+    if "parity_candidate" in w.extra:
+        c = w.extra["candidates"]
+        PA = conditioned_parity_matrix(w.n, w.k, w.seed, c, STREAM_P, pick=w.extra["parity_candidate"])[0]
+        PT = conditioned_parity_matrix(w.n, w.k, w.seed, c, STREAM_PT, pick=w.extra["parity_candidate_T"])[0]
+        return PA, PT, w.extra["planes"]
+    return parity_matrix(w.n, w.k, w.seed), parity_matrix(w.n, w.k, w.seed, STREAM_PT), 2

@@ -536,3 +536,42 @@ def test_conditioned_generator_single_plane_every_survivor_set(lib, torch):
         worst[name] = float(np.max(np.max(np.abs(got - ref[None, :]), axis=1)) / np.max(np.abs(ref)))
     assert worst["conditioned"] <= TOL_F32, worst
     assert worst["plain"] > worst["conditioned"], worst
+
+
+@pytest.mark.parametrize("which", ["A", "T"])
+def test_conditioned_gd_codes_single_plane_every_survivor_set(lib, torch, which):
+    """The coded gradient-descent codes' certified (20,16) generators with one fp32
+    parity plane: every one of the C(20,16) = 4845 survivor sets decodes A x
+    within the fp32 tolerance (code of A and code of A^T, each on its own
+    matrix).  The plain draw of the code of A (worst decode system 62 times worse
+    conditioned) misses the tolerance on its worst set."""
+    w = synth.WORKLOADS["gd20x16_conditioned_262144x4096"]
+    n, k, q, r = w.n, w.k, 16000, 2048
+    PA, PT, planes = synth.gd_codes(w)
+    Pc = PA if which == "A" else PT
+    A = synth.gaussian((q, r), 43, synth.STREAM_A)
+    x = synth.gaussian((r,), 43, synth.STREAM_X)
+    ref = oc.plain_product(A, x[:, None])[:, 0]
+    sets = np.array(list(itertools.combinations(range(n), k)), dtype=np.int32)
+    dA, dx, dsets = torch.from_numpy(A).cuda(), torch.from_numpy(x).cuda(), torch.from_numpy(sets).cuda()
+    cands = [("conditioned", Pc)]
+    if which == "A":
+        cands.append(("plain", synth.parity_matrix(n, k, w.seed)))
+    worst = {}
+    for name, P in cands:
+        code = lib.Code.systematic(P, planes)
+        par = lib.alloc_parity(code, q, r, torch.float32)
+        lib.coded_encode(code, dA, par)
+        Y = lib.alloc_y(code, q, 1, torch.float64)
+        lib.coded_worker_mm(code, dA, par, dx, Y)
+        out = torch.empty((len(sets), q), dtype=torch.float32, device="cuda")
+        info = info_tensor(torch, len(sets))
+        lib.coded_decode_batched(code, dsets, Y, q, out, info)
+        torch.cuda.synchronize()
+        assert np.all(info.cpu().numpy() == 0)
+        got = out.cpu().numpy()
+        worst[name] = float(np.max(np.max(np.abs(got - ref[None, :]), axis=1)) / np.max(np.abs(ref)))
+    print(f"one plane, every survivor set of the code of {which}: worst normwise error {worst}")
+    assert worst["conditioned"] <= TOL_F32, worst
+    if "plain" in worst:
+        assert worst["plain"] > TOL_F32, worst

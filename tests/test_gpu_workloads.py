@@ -95,11 +95,13 @@ def test_decode_heavy_workload_full_size(lib, torch):
         assert float(np.max(np.max(np.abs(got - ref_b), axis=0) / den)) <= TOL_F32
 
 
-def test_gd_workload_full_size(lib, torch):
+@pytest.mark.parametrize("name", ["gd20x16_262144x4096", "gd20x16_conditioned_262144x4096"])
+def test_gd_workload_full_size(lib, torch, name):
     """(20,16) codes for A (262144 x 4096, N(0, 1/4096)) and A^T: sampled iterations against the plain
     fp64 update of the same iterate, survivors against the oracle, and first-order optimality after
-    the 200 iterations of the workload."""
-    w = synth.WORKLOADS["gd20x16_262144x4096"]
+    the 200 iterations of the workload.  The configured recipe (plain draws, two planes) and the
+    certified generators with one parity plane."""
+    w = synth.WORKLOADS[name]
     n, k, q, r, seed = w.n, w.k, w.q, w.r, w.seed
     A = synth.gaussian_rows(q, r, seed, synth.STREAM_A, std=w.a_std)
     wstar = synth.gaussian((r,), seed, synth.STREAM_WSTAR)
@@ -107,8 +109,9 @@ def test_gd_workload_full_size(lib, torch):
     y = (A64 @ wstar.astype(np.float64) + w.extra["noise_std"] * synth.gaussian((q,), seed, synth.STREAM_NOISE)
          ).astype(np.float32)
     eta = w.extra["eta"] / (q * w.a_std ** 2)
-    cA = lib.Code.systematic(synth.parity_matrix(n, k, seed), 2)
-    cT = lib.Code.systematic(synth.parity_matrix(n, k, seed, synth.STREAM_PT), 2)
+    PA, PT, planes = synth.gd_codes(w)
+    cA = lib.Code.systematic(PA, planes)
+    cT = lib.Code.systematic(PT, planes)
     dA = torch.from_numpy(A).cuda()
     dAT = torch.empty((r, q), dtype=torch.float32, device="cuda")
     lib.coded_transpose(dA, dAT)

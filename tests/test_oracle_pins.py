@@ -371,6 +371,30 @@ def test_coded_gd_tracks_plain_gd_and_reaches_least_squares():
     assert np.allclose(rec[-1], x_ls, rtol=1e-6, atol=1e-8)
 
 
+@pytest.mark.parametrize("which", ["A", "T"])
+def test_conditioned_gd_generators_certificate(which):
+    """The coded gradient-descent codes' certified generators (code of A and of
+    A^T): every one of the C(20,16) = 4845 survivor sets has a decode system
+    with condition number at most the recorded bound, which is attained, and
+    the plain draw of the same stream is worse."""
+    w = synth.WORKLOADS["gd20x16_conditioned_262144x4096"]
+    PA, PT, planes = synth.gd_codes(w)
+    assert planes == 1
+    P = PA if which == "A" else PT
+    bound = w.extra["worst_condition" if which == "A" else "worst_condition_T"]
+    G = oc.systematic_generator(P)
+    k = w.k
+    seen = 0.0
+    for S in itertools.combinations(range(w.n), k):
+        par = [i for i in S if i >= k]
+        miss = [j for j in range(k) if j not in S]
+        if par:
+            seen = max(seen, np.linalg.cond(G[np.array(par)][:, miss]))
+    assert abs(seen - bound) <= 0.05 and abs(synth.worst_decode_condition(P) - seen) <= 1e-6 * seen
+    plain = synth.parity_matrix(w.n, w.k, w.seed, synth.STREAM_P if which == "A" else synth.STREAM_PT)
+    assert synth.worst_decode_condition(plain) > 2 * bound
+
+
 def test_conditioned_generator_certificate():
     """The GEMV regime's conditioned generator: every one of the C(16,12) survivor
     sets of G = [I; P] has a decode system (parity survivors x missing blocks)
