@@ -1001,9 +1001,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true",
                     help="default workload: skip the dense bf16 sub-record (the GEMM half of the metric)")
-    ap.add_argument("--cpu-products", type=int, default=300)
+    ap.add_argument("--cpu-products", type=int, default=700)
     ap.add_argument("--cpu-decodes", type=int, default=1000)
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-rows", type=int, default=3072)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--time-unit-us", type=float, default=10000.0,
                     help="straggler workload: microseconds per unit of the runtime model")
