@@ -1005,6 +1005,8 @@ def main():
     ap.add_argument("--cpu-decodes", type=int, default=1000)
     ap.add_argument("--cpu-rows", type=int, default=3072)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="measure the device ceilings (read/write bandwidth, row-window reads, matrix rates) and exit")
     ap.add_argument("--time-unit-us", type=float, default=10000.0,
                     help="straggler workload: microseconds per unit of the runtime model")
     args = ap.parse_args()
@@ -1014,6 +1016,12 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy, 5)
+        return
+    if args.calibrate:
+        from paper_1512_02673_amd import build as _build, calib
+        if not os.path.exists(_build.CALIB_PATH):
+            _build.build_calib()
+        print(json.dumps(calib.ceilings()), flush=True)
         return
     import torch
     if not torch.cuda.is_available():

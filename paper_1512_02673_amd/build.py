@@ -50,6 +50,25 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
+CALIB_SRC = os.path.join(PKG, "calib", "ceilings.hip")
+CALIB_PATH = os.path.join(PKG, "libcoded_calib.so")
+
+
+def build_calib(verbose: bool = False) -> str:
+    """Compile the device-ceiling probes (calib/ceilings.hip) into their own library."""
+    tmp = CALIB_PATH + ".tmp"
+    # Matrix-instruction operands kept in vector registers: the rate probes'
+    # accumulators are then not copied between register files every iteration.
+    cmd = [hipcc(), "-x", "hip", *DEVICE, "-mllvm", "-amdgpu-mfma-vgpr-form=1", *COMMON, "-shared", CALIB_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"compiling {CALIB_SRC} failed:\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, CALIB_PATH)
+    return CALIB_PATH
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source and link the shared library; returns its path."""
     os.makedirs(BUILD, exist_ok=True)
@@ -64,6 +83,7 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"linking {LIB_NAME} failed:\n{res.stdout}\n{res.stderr}")
     os.replace(tmp, LIB_PATH)
+    build_calib(verbose)
     return LIB_PATH
 
 

@@ -2,6 +2,7 @@
 every function the header declares, and its host logic (the survivor draw)
 agrees bit for bit with the oracle."""
 import ctypes
+import os
 
 import numpy as np
 import pytest
@@ -167,3 +168,13 @@ def test_code_device_buffer_is_the_callers(lib):
     assert "device_buf" in lib.last_error()
     with pytest.raises(lib.CodedError):
         lib.coded_code_bytes(2, 3)
+
+
+def test_calibration_library_exports_its_probes():
+    """The device-ceiling probes (calib/ceilings.hip) build into their own library with four entry points."""
+    from paper_1512_02673_amd import build as _build
+    if not os.path.exists(_build.CALIB_PATH):
+        _build.build_calib()
+    h = ctypes.CDLL(_build.CALIB_PATH)
+    for name in ("calib_read", "calib_write", "calib_read_rows", "calib_rate"):
+        assert hasattr(h, name), name
