@@ -264,13 +264,17 @@ def gemv_workload(args):
     matmul_ms = elapsed * 1e3 / K
 
     qb = code.qb(q)
-    algo_bytes = 4.0 * q * r + 4.0 * code.planes * (n - k) * qb * r + 4.0 * r + 8.0 * n * qb
+    lo16 = planes == lib.CODED_PLANES_LO_BF16
+    # bytes per parity element: fp32 planes, or an fp32 hi and a bf16 lo plane
+    par_elem = 6.0 if lo16 else 4.0 * planes
+    algo_bytes = 4.0 * q * r + par_elem * (n - k) * qb * r + 4.0 * r + 8.0 * n * qb
     gemv_mean_ms = float(gemv_ms.mean())
     achieved = algo_bytes / (gemv_mean_ms * 1e-3) / 1e9
+    kname = f"gemv_wg_kernel<4, 8, 256, {'true' if lo16 else 'false'}>"
     if w.name == "gemv16x12_65536x8192":
         traffic = measured_traffic(algo_bytes)
     else:
-        traffic = measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 8, 256>", algo_bytes)
+        traffic = measured_kernel_traffic(w.name, kname, algo_bytes)
     result = {
         "metric": METRIC,
         "value": K / elapsed,
@@ -285,14 +289,15 @@ def gemv_workload(args):
         "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "s": 1, "input_dtype": "f32",
-                   "parity_planes": code.planes, "worker_accumulate": "f64", "encode": "once, before timing",
+                   "parity_planes": ("fp32 hi + bf16 lo (6 bytes per element)" if lo16 else planes),
+                   "worker_accumulate": "f64", "encode": "once, before timing",
                    "survivors": "fresh shifted-exponential draw per product (shift 1, rate 1)"},
         "encode_ms": encode_ms,
         "gemv_ms_mean": gemv_mean_ms,
         "gemv_ms_p5_p95": [float(np.percentile(gemv_ms, 5)), float(np.percentile(gemv_ms, 95))],
         "decode_ms_mean": float(dec_ms.mean()),
         "coded_matmul_ms_per_call": matmul_ms,
-        "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": kname, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "algorithmic_bytes_per_launch": algo_bytes,
                      "traffic": traffic, "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE)"},
@@ -614,8 +619,8 @@ def gd_workload(args):
         "roofline": {"bound": "hbm", "kernel": "gemv_wg_kernel (A and A^T launches)", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "algorithmic_bytes_per_launch": [bA, bT],
-                     "traffic": [measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 4, 256>", bA),
-                                 measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 8, 256>", bT)],
+                     "traffic": [measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 4, 256, false>", bA),
+                                 measured_kernel_traffic(w.name, "gemv_wg_kernel<4, 8, 256, false>", bT)],
                      "step_frac": (bA + bT) / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
     }
     return result
@@ -994,7 +999,8 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="gemv16x12_65536x8192",
-                    choices=["gemv16x12_65536x8192", "gemv16x12_conditioned_65536x8192", "mds4x2_2048x512",
+                    choices=["gemv16x12_65536x8192", "gemv16x12_conditioned_65536x8192",
+                             "gemv16x12_bf16lo_65536x8192", "mds4x2_2048x512",
                              "decode64x48_16384x4096x8", "gd20x16_262144x4096", "gd20x16_conditioned_262144x4096",
                              "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
                              "straggler16x12_65536x8192", "shuffle16_1000000x256"])

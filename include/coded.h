@@ -26,7 +26,11 @@
  *    the exact-sum pair hi + lo: hi is the coded value rounded to the storage
  *    dtype and lo the rounded remainder, which gives the parity blocks about
  *    twice the storage precision at (n-k)/n extra bytes.  planes == 1 stores
- *    hi only.
+ *    hi only.  With CODED_PLANES_LO_BF16 (fp32 inputs) the hi plane is fp32
+ *    and the lo plane bfloat16: hi as above, then at byte offset
+ *    4*(n-k)*qb*r the lo plane's uint16 elements [p*qb*r + t*r + c] (about
+ *    32 significant bits in all; 6 instead of 8 bytes per parity element).
+ *    For bf16 inputs it is the same layout as planes == 2.
  *  - Y (worker results) is n x qb x s, dense: element (i, t, c) at
  *    [(i*qb + t)*s + c].  Rows t with i*qb + t >= q of systematic blocks are
  *    the zero padding and hold 0.
@@ -70,6 +74,9 @@ typedef enum coded_dtype {
 /* Largest n supported (survivor and worker lists travel as kernel arguments). */
 #define CODED_MAX_N 128
 
+/* Parity storage with an fp32 hi plane and a bfloat16 lo plane (see above). */
+#define CODED_PLANES_LO_BF16 3
+
 /* Opaque (n,k) code: the generator G on host and device. */
 typedef struct coded_code coded_code;
 
@@ -89,7 +96,13 @@ coded_status coded_code_bytes(int32_t n, int32_t k, int64_t* bytes);
  *             is responsible for G being MDS (every k x k row subset
  *             invertible); a set that is not invertible is reported at
  *             decode time through info.
- *   planes    parity storage planes: 2 (hi + lo, default recipe) or 1.
+ *   planes    parity storage: 2 (hi + lo, default recipe), 1 (hi only) or
+ *             CODED_PLANES_LO_BF16 (fp32 hi + bfloat16 lo, for the
+ *             HBM-bound single-vector product: 6 bytes per parity element).
+ *             With that mode fp32 products with s > 1 run the general
+ *             vector kernel instead of the matrix cores, and coded_matmul
+ *             does not take its single-launch path for small problems;
+ *             results keep the same bounds.
  *   device_buf, device_buf_bytes
  *             caller-owned device memory of the current device, 16-byte
  *             aligned, at least coded_code_bytes(n, k) bytes (else
@@ -109,7 +122,8 @@ coded_status coded_code_info(const coded_code* code, int32_t* n, int32_t* k, int
 /*
  * coded_sizes -- bytes of the caller-allocated buffers for an A of q x r,
  * X of r x s, compute dtype dt and worker-result dtype y_dt.
- *   parity_bytes     the parity buffer (planes * (n-k) * qb * r elements of dt)
+ *   parity_bytes     the parity buffer (planes * (n-k) * qb * r elements of dt;
+ *                    CODED_PLANES_LO_BF16 with fp32: 6 * (n-k) * qb * r bytes)
  *   y_bytes          Y (n * qb * s elements of y_dt)
  *   workspace_bytes  workspace of coded_matmul (its Y, in y_dt = F64 for F32
  *                    inputs and F32 for BF16 inputs, followed by the worker

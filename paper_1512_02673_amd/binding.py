@@ -20,6 +20,7 @@ CODED_OK, CODED_ERR_ARG, CODED_ERR_SHAPE, CODED_ERR_TOO_FEW, CODED_ERR_SINGULAR,
 CODED_F32, CODED_BF16, CODED_F64 = 0, 1, 2
 CODED_MAX_N = 128
 CODED_NOALLOC_SCRATCH_BYTES = 64 << 20
+CODED_PLANES_LO_BF16 = 3   # fp32 codes: hi plane fp32, lo plane bfloat16
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "coded.h")
 
@@ -407,9 +408,27 @@ def coded_simulate_runtimes(n: int, k: int, seed: int, first_draw: int, t_uncode
 # ---------------------------------------------------------------- buffer helpers
 
 def alloc_parity(code: Code, q: int, r: int, dtype, device="cuda"):
+    """Parity planes of a q x r input: (planes, n-k, qb, r) of `dtype`; for a
+    CODED_PLANES_LO_BF16 code (fp32 only) a flat uint8 buffer holding the fp32
+    hi plane followed by the bfloat16 lo plane (see parity_planes)."""
     torch = _torch()
     qb = code.qb(q)
+    if code.planes == CODED_PLANES_LO_BF16:
+        if dtype != torch.float32:
+            raise ValueError("a bfloat16 lo plane is for fp32 inputs")
+        return torch.empty(6 * (code.n - code.k) * qb * r, dtype=torch.uint8, device=device)
     return torch.empty((code.planes, code.n - code.k, qb, r), dtype=dtype, device=device)
+
+
+def parity_planes(code: Code, par, q: int, r: int):
+    """(hi, lo) views of a CODED_PLANES_LO_BF16 parity buffer: hi float32 and
+    lo bfloat16, each (n-k, qb, r)."""
+    torch = _torch()
+    shape = (code.n - code.k, code.qb(q), r)
+    hb = 4 * shape[0] * shape[1] * shape[2]
+    hi = par[:hb].view(torch.float32).view(shape)
+    lo = par[hb:].view(torch.bfloat16).view(shape)
+    return hi, lo
 
 
 def alloc_y(code: Code, q: int, s: int, dtype, device="cuda"):

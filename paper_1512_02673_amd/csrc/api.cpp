@@ -143,7 +143,7 @@ coded_status do_encode(const coded_code* c, coded_dtype dt, const void* A, int64
     if (single_pass_bf16(c, dt, A, q, r, lda, parity)) {
         e = launch_fused_bf16(fused_args(c, A, q, r, lda, parity, nullptr, nullptr), false, c->compute_units, st);
     } else {
-        EncodeArgs a{A, parity, c->dG, q, r, lda, qb, c->n, c->k, c->planes};
+        EncodeArgs a{A, parity, c->dG, q, r, lda, qb, c->n, c->k, c->planes, c->lo_bf16 && dt == CODED_F32};
         e = dt == CODED_F32 ? launch_encode_f32(a, st) : launch_encode_bf16(a, st);
     }
     if (e != hipSuccess) return hip_fail(e, "encode launch");
@@ -181,6 +181,7 @@ coded_status do_workers(const coded_code* c, coded_dtype dt, const void* A, int6
     a.n = c->n;
     a.k = c->k;
     a.planes = c->planes;
+    a.lo_bf16 = c->lo_bf16 && dt == CODED_F32;
     a.y_f64 = y_dt == CODED_F64;
     a.xt = dt == CODED_BF16 ? workspace : nullptr;
     a.xt_ready = xt_ready ? 1 : 0;
@@ -308,7 +309,8 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
     *out = nullptr;
     if (!G) return fail(CODED_ERR_ARG, "G is NULL");
     if (k < 1 || n < k || n > CODED_MAX_N) return fail(CODED_ERR_ARG, "need 1 <= k <= n <= CODED_MAX_N");
-    if (planes != 1 && planes != 2) return fail(CODED_ERR_ARG, "planes must be 1 or 2");
+    if (planes != 1 && planes != 2 && planes != CODED_PLANES_LO_BF16)
+        return fail(CODED_ERR_ARG, "planes must be 1, 2 or CODED_PLANES_LO_BF16");
     for (int64_t i = 0; i < static_cast<int64_t>(n) * k; ++i)
         if (!std::isfinite(G[i])) return fail(CODED_ERR_ARG, "G has a non-finite entry");
     for (int i = 0; i < k; ++i)
@@ -333,7 +335,8 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
     auto* c = new coded_code();
     c->n = n;
     c->k = k;
-    c->planes = planes;
+    c->planes = planes == CODED_PLANES_LO_BF16 ? 2 : planes;
+    c->lo_bf16 = planes == CODED_PLANES_LO_BF16;
     c->device = dev;
     c->G.assign(G, G + static_cast<size_t>(n) * k);
     c->dG = static_cast<double*>(device_buf);
@@ -369,7 +372,7 @@ coded_status coded_code_info(const coded_code* c, int32_t* n, int32_t* k, int32_
     if (!c) return fail(CODED_ERR_ARG, "code is NULL");
     if (n) *n = c->n;
     if (k) *k = c->k;
-    if (planes) *planes = c->planes;
+    if (planes) *planes = c->lo_bf16 ? CODED_PLANES_LO_BF16 : c->planes;
     return CODED_OK;
 }
 
@@ -382,7 +385,8 @@ coded_status coded_sizes(const coded_code* c, coded_dtype dt, coded_dtype y_dt, 
     if (q < 0 || r < 0 || s < 0) return fail(CODED_ERR_SHAPE, "q, r, s must be >= 0");
     const int64_t qb = block_rows(q, c->k);
     if (parity_bytes)
-        *parity_bytes = static_cast<int64_t>(c->planes) * (c->n - c->k) * qb * r * static_cast<int64_t>(dtype_size(dt));
+        *parity_bytes = (c->lo_bf16 && dt == CODED_F32 ? 6 : static_cast<int64_t>(c->planes) * dtype_size(dt)) *
+                        (c->n - c->k) * qb * r;
     if (y_bytes) *y_bytes = static_cast<int64_t>(c->n) * qb * s * static_cast<int64_t>(dtype_size(y_dt));
     const int64_t wws = dt == CODED_BF16 ? worker_workspace_bytes_bf16(r, s) : 0;
     if (workspace_bytes) *workspace_bytes = matmul_y_bytes(c, dt, q, s) + wws;
@@ -542,7 +546,7 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
     if (ldx < std::max<int64_t>(s, 1)) return fail(CODED_ERR_SHAPE, "ldx must be >= max(s, 1)");
 
     void* wws = static_cast<char*>(workspace) + matmul_y_bytes(c, dt, q, s);
-    if (dt == CODED_F32 && s == 1 && ldx == 1 && c->n > c->k && A && X && parity &&
+    if (dt == CODED_F32 && s == 1 && ldx == 1 && c->n > c->k && A && X && parity && !c->lo_bf16 &&
         onepass_supported(c->n, c->k, q, r, lda, A, parity, X)) {
         // small problem: encode (unless ready), products and decode in one launch
         OnePassArgs oa{};

@@ -76,6 +76,8 @@ __global__ __launch_bounds__(kThreads) void encode_f32_kernel(EncodeArgs a, int6
 
     float* par = static_cast<float*>(a.parity);
     const int64_t plane = static_cast<int64_t>(npar) * a.qb * a.r;
+    // lo plane as bfloat16: after the fp32 hi plane, same element order
+    uint16_t* par16 = reinterpret_cast<uint16_t*>(par + plane);
 #pragma unroll
     for (int p = 0; p < kGroup; ++p) {
         if (p >= np) break;
@@ -83,17 +85,32 @@ __global__ __launch_bounds__(kThreads) void encode_f32_kernel(EncodeArgs a, int6
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             hi[v] = static_cast<float>(acc[p][v]);
-            lo[v] = static_cast<float>(acc[p][v] - static_cast<double>(hi[v]));
+            lo[v] = static_cast<float>(acc[p][v] - static_cast<double>(hi[v]));   // exact remainder, rounded to fp32
         }
-        float* dst = par + (static_cast<int64_t>(p0 + p) * a.qb + t) * a.r + c;
+        const int64_t off = (static_cast<int64_t>(p0 + p) * a.qb + t) * a.r + c;
+        float* dst = par + off;
         if constexpr (VEC == 4) {
             *reinterpret_cast<float4*>(dst) = make_float4(hi[0], hi[1], hi[2], hi[3]);
-            if (a.planes == 2) *reinterpret_cast<float4*>(dst + plane) = make_float4(lo[0], lo[1], lo[2], lo[3]);
+            if (a.planes == 2) {
+                if (a.lo_bf16) {
+                    uint2 l;
+                    l.x = f32_to_bf16_rne(lo[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(lo[1])) << 16);
+                    l.y = f32_to_bf16_rne(lo[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(lo[3])) << 16);
+                    *reinterpret_cast<uint2*>(par16 + off) = l;
+                } else {
+                    *reinterpret_cast<float4*>(dst + plane) = make_float4(lo[0], lo[1], lo[2], lo[3]);
+                }
+            }
         } else {
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
                 dst[v] = hi[v];
-                if (a.planes == 2) dst[plane + v] = lo[v];
+                if (a.planes == 2) {
+                    if (a.lo_bf16)
+                        par16[off + v] = f32_to_bf16_rne(lo[v]);
+                    else
+                        dst[plane + v] = lo[v];
+                }
             }
         }
     }

@@ -11,6 +11,7 @@
 
 struct coded_code {
     int32_t n = 0, k = 0, planes = 2;
+    bool lo_bf16 = false;      // CODED_PLANES_LO_BF16: planes == 2, the lo plane stored as bfloat16 for fp32 inputs
     std::vector<double> G;     // host copy, n*k row-major
     double* dG = nullptr;      // device copy, n*k row-major (in the caller's buffer)
     float* dPf = nullptr;      // device copy of the parity rows P ((n-k) x k) in fp32 (same buffer)
@@ -41,6 +42,7 @@ struct EncodeArgs {
     const double* G;      // device n x k
     int64_t q, r, lda, qb;
     int32_t n, k, planes;
+    int32_t lo_bf16;      // fp32 with planes == 2: lo plane stored as bfloat16
 };
 hipError_t launch_encode_f32(const EncodeArgs& a, hipStream_t st);
 hipError_t launch_encode_bf16(const EncodeArgs& a, hipStream_t st);
@@ -57,6 +59,7 @@ struct WorkerArgs {
     int32_t n_sys, n_par; // active systematic / parity workers
     void* xt;             // bf16 only: scratch for X transposed (s x r), or null
     int32_t xt_ready;     // bf16 only: xt already holds X transposed (skip the transpose)
+    int32_t lo_bf16;      // fp32 with planes == 2: the lo plane is bfloat16 (after the fp32 hi plane)
     uint8_t sys_ids[kMaxN];
     uint8_t par_ids[kMaxN];
 };

@@ -28,14 +28,37 @@ __device__ inline float4 load_stream(const float* p) {
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
+// Four bfloat16 values (8 bytes, streamed) as raw bits, and their exact
+// widening to fp32 (kept apart so a select can take the raw load).
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+__device__ inline u32x2 load_stream_bf16x4(const uint16_t* p) {
+    // a global-memory pointer, so the load is a global (not flat) load
+    typedef const __attribute__((address_space(1))) u32x2* gptr;
+    return __builtin_nontemporal_load((gptr)(p));
+}
+__device__ inline float4 widen_bf16x4(u32x2 v) {
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u));
+}
+
+__device__ inline float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// First element of the lo plane when it is stored as bfloat16: directly after
+// the fp32 hi plane, in the same (worker, block row, column) order.
+__device__ inline const uint16_t* lo16_base(const WorkerArgs& a) {
+    return reinterpret_cast<const uint16_t*>(static_cast<const float*>(a.parity) +
+                                             static_cast<int64_t>(a.n - a.k) * a.qb * a.r);
+}
+
 struct RowRef {
-    const float* ptr;   // start of the plane row (null: zero padding / out of range)
-    int64_t t;          // block row
+    const float* ptr;     // start of the plane row (null: zero padding / out of range)
+    const uint16_t* p16;  // instead of ptr for a bfloat16 lo plane
+    int64_t t;            // block row
 };
 
 // Plane row `pr` of worker `w`.
 __device__ inline RowRef plane_row(const WorkerArgs& a, int w, int64_t pr, bool parity) {
-    RowRef rr{nullptr, 0};
+    RowRef rr{nullptr, nullptr, 0};
     if (!parity) {
         rr.t = pr;
         const int64_t row = static_cast<int64_t>(w) * a.qb + pr;
@@ -46,8 +69,11 @@ __device__ inline RowRef plane_row(const WorkerArgs& a, int w, int64_t pr, bool 
         rr.t = t;
         if (t < a.qb) {
             const int64_t plane = static_cast<int64_t>(a.n - a.k) * a.qb * a.r;
-            rr.ptr = static_cast<const float*>(a.parity) + h * plane +
-                     (static_cast<int64_t>(w - a.k) * a.qb + t) * a.r;
+            const int64_t off = (static_cast<int64_t>(w - a.k) * a.qb + t) * a.r;
+            if (h == 1 && a.lo_bf16)
+                rr.p16 = lo16_base(a) + off;
+            else
+                rr.ptr = static_cast<const float*>(a.parity) + h * plane + off;
         }
     }
     return rr;
@@ -61,7 +87,9 @@ __device__ inline RowRef plane_row(const WorkerArgs& a, int w, int64_t pr, bool 
 // NT*4*XR are swept in column chunks (x reloaded per chunk).  A parity row's
 // planes (hi, lo) are summed into the same fp64 accumulator.  Partial sums
 // are combined across lanes (shuffles) and waves (LDS) in a fixed order.
-template <int T, int XR, int NT>
+// LO16: the lo plane is bfloat16 (8-byte loads of four values, widened
+// exactly to fp32, so the products stay exact in fp64).
+template <int T, int XR, int NT, bool LO16>
 __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
     constexpr int NW = NT / 64;
     constexpr int kChunk = NT * 4 * XR;
@@ -92,18 +120,26 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
 
     // Row pointers of the tile (null: padding row or beyond the block).
     const float* rows[T][2];
+    const uint16_t* lo16[T];
 #pragma unroll
     for (int i = 0; i < T; ++i) {
         const int64_t t = t0 + i;
         rows[i][0] = rows[i][1] = nullptr;
+        lo16[i] = nullptr;
         if (t >= a.qb) continue;
         if (!parity) {
             const int64_t rr = static_cast<int64_t>(worker) * a.qb + t;
             if (rr < a.q) rows[i][0] = static_cast<const float*>(a.A) + rr * a.lda;
         } else {
-            const float* base = static_cast<const float*>(a.parity) + (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
+            const int64_t off = (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
+            const float* base = static_cast<const float*>(a.parity) + off;
             rows[i][0] = base;
-            if (nplanes == 2) rows[i][1] = base + plane;
+            if (nplanes == 2) {
+                if constexpr (LO16)
+                    lo16[i] = lo16_base(a) + off;
+                else
+                    rows[i][1] = base + plane;
+            }
         }
     }
 
@@ -123,12 +159,29 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const float* row = rows[i][h];
-                if (!row) continue;
+                const bool bf = LO16 && h == 1;
+                if (bf ? !lo16[i] : !row) continue;
                 float4 av[XR];
 #pragma unroll
                 for (int j = 0; j < XR; ++j) {
                     const int64_t c = cb + tid * 4 + j * NT * 4;
+                    // selects, not branches, so the loads stay in flight together
+                    if constexpr (LO16) {
+                        if (h == 1) continue;
+                    }
                     av[j] = c < a.r ? load_stream(row + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+                if constexpr (LO16) {
+                    if (h == 1) {
+                        u32x2 raw[XR];
+#pragma unroll
+                        for (int j = 0; j < XR; ++j) {
+                            const int64_t c = cb + tid * 4 + j * NT * 4;
+                            raw[j] = c < a.r ? load_stream_bf16x4(lo16[i] + c) : u32x2{0u, 0u};
+                        }
+#pragma unroll
+                        for (int j = 0; j < XR; ++j) av[j] = widen_bf16x4(raw[j]);
+                    }
                 }
 #pragma unroll
                 for (int j = 0; j < XR; ++j) {
@@ -173,10 +226,10 @@ __global__ __launch_bounds__(kThreads) void gemm_small_f32_kernel(WorkerArgs a) 
 #pragma unroll
         for (int j = 0; j < SC; ++j) acc[j] = 0.0;
         for (int h = 0; h < nplanes; ++h) {
-            const float* rowp = plane_row(a, worker, parity ? t * a.planes + h : t, parity).ptr;
-            if (!rowp) continue;
+            const RowRef rr = plane_row(a, worker, parity ? t * a.planes + h : t, parity);
+            if (!rr.ptr && !rr.p16) continue;
             for (int64_t c = lane; c < a.r; c += 64) {
-                const double av = rowp[c];
+                const double av = rr.p16 ? bf16_bits_to_f32(rr.p16[c]) : rr.ptr[c];
                 const float* xr = x + c * a.ldx + c0;
 #pragma unroll
                 for (int j = 0; j < SC; ++j)
@@ -212,7 +265,12 @@ hipError_t launch_gemv_wg(const WorkerArgs& a, hipStream_t st) {
     const int64_t blocks = ceil_div(a.qb, T) * (a.n_sys + a.n_par);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, a);
+    if (a.lo_bf16 && a.planes == 2)
+        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, true>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
+                           a);
+    else
+        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, false>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                           st, a);
     return hipGetLastError();
 }
 

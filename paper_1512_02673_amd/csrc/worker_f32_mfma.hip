@@ -290,8 +290,9 @@ hipError_t launch_mm(const WorkerArgs& a, int64_t c0, hipStream_t st) {
 }  // namespace
 
 bool gemm_f32_mfma_supported(const WorkerArgs& a) {
-    // K positions are 32-bit inside the kernel; rows need 16-byte alignment.
-    return a.s > 1 && a.r > 0 && a.r % 4 == 0 && a.r <= (1ll << 30) && a.lda % 4 == 0 &&
+    // K positions are 32-bit inside the kernel; rows need 16-byte alignment;
+    // planes are fp32 (a bfloat16 lo plane takes the general kernel).
+    return a.s > 1 && !a.lo_bf16 && a.r > 0 && a.r % 4 == 0 && a.r <= (1ll << 30) && a.lda % 4 == 0 &&
            (reinterpret_cast<uintptr_t>(a.A) & 15u) == 0 && (reinterpret_cast<uintptr_t>(a.parity) & 15u) == 0;
 }
 

@@ -40,6 +40,10 @@ WORKLOADS = {
                                                  "f32", 2, 1000,
                                                  extra={"parity_candidate": 2841, "candidates": 3000,
                                                         "worst_condition": 679.2, "planes": 1}),
+    # The GEMV workload with 6-byte parity elements: the fp32 hi plane and a
+    # bfloat16 lo plane (planes code 3), same generator and inputs.
+    "gemv16x12_bf16lo_65536x8192": Workload("gemv16x12_bf16lo_65536x8192", 16, 12, 65536, 8192, 1, "f32", 2, 1000,
+                                            extra={"planes": 3}),
     "gemm_bf16_32x24_131072x16384x64": Workload("gemm_bf16_32x24_131072x16384x64", 32, 24, 131072, 16384,
                                                 64, "bf16", 3, 20),
     "decode64x48_16384x4096x8": Workload("decode64x48_16384x4096x8", 64, 48, 16384, 4096, 8, "f32", 4, 10000,

@@ -152,6 +152,12 @@ def test_noalloc_scratch_size_matches_header(lib):
     assert lib.CODED_NOALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
 
 
+def test_planes_constant_matches_header(lib):
+    import re
+    m = re.search(r"#define\s+CODED_PLANES_LO_BF16\s+(\d+)", open(lib.HEADER).read())
+    assert m and lib.CODED_PLANES_LO_BF16 == int(m.group(1))
+
+
 def test_code_device_buffer_is_the_callers(lib):
     """coded_code_bytes sizes the caller's buffer (G in fp64, then P in fp32, each
     256-byte aligned); coded_code_create refuses a missing or short buffer before
