@@ -476,7 +476,11 @@ def decode_workload(args):
     qb = code.qb(q)
     prod_bytes = 4.0 * q * r + 4.0 * code.planes * (n - k) * qb * r + 4.0 * r * s + 8.0 * n * qb * s
     prod_flops = 2.0 * (k * qb + code.planes * (n - k) * qb) * r * s
-    sets, _ = lib.coded_draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
+    if args.exact_parity is None:
+        sets, _ = lib.coded_draw_survivor_sets(n, k, seed, B, min_parity=w.extra["min_parity"])
+    else:
+        # cost against the number of missing blocks: every set has exactly that many
+        sets = synth.exact_parity_sets(n, k, args.exact_parity, B, seed)
     dsets = torch.from_numpy(sets).cuda()
     out = torch.empty((B, q, s), dtype=torch.float32, device="cuda")
     info = torch.zeros(B, dtype=torch.int32, device="cuda")
@@ -503,12 +507,16 @@ def decode_workload(args):
         "metric": METRIC, "value": B * K / elapsed, "unit": "decodes/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": elapsed * 1e3 / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64", "data": "synthetic",
+        "launch_ms_mean": float(ms.mean()), "launch_ms_p5_p50_p95": [float(np.percentile(ms, p)) for p in (5, 50, 95)],
         "config": {"workload": w.name, "n": n, "k": k, "q": q, "r": r, "s": s, "sets_per_step": B,
-                   "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean())},
+                   "min_parity": w.extra["min_parity"], "mean_parity_survivors": float(m.mean()),
+                   "sets": ("distinct drawn sets (shifted-exponential runtimes) with >= min_parity parity survivors"
+                            if args.exact_parity is None else
+                            f"uniform random sets with exactly {args.exact_parity} parity survivors (repeats allowed)")},
         "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
-                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
-                     "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double>")},
+                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double, true>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
+                     "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double, true>")},
         "products": {"kernel": "gemm_f32_mfma_kernel<1, 2, true, 64, 4> (64 worker products, s = 8, once per run)",
                      "ms_mean": float(prod_ms.mean()), "ms_min": float(prod_ms.min()),
                      "algorithmic_bytes_per_launch": prod_bytes,
@@ -1005,6 +1013,10 @@ def main():
                              "gemm_bf16_32x24_131072x16384x64", "runtime_sim_10x5",
                              "straggler16x12_65536x8192", "shuffle16_1000000x256"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--exact-parity", type=int, default=None, metavar="M",
+                    help="decode workload: survivor sets with exactly M parity survivors instead of the drawn sets")
+    ap.add_argument("--no-lo-plane", action="store_true",
+                    help="default workload: skip the sub-record of the same products with a bfloat16 lo plane")
     ap.add_argument("--no-dense", action="store_true",
                     help="default workload: skip the dense bf16 sub-record (the GEMM half of the metric)")
     ap.add_argument("--cpu-products", type=int, default=700)
@@ -1039,9 +1051,9 @@ def main():
         result = mds_small_workload(args)
     elif args.workload == "decode64x48_16384x4096x8":
         if "--steps" not in sys.argv:
-            args.steps = 20
+            args.steps = 30
         if "--warmup" not in sys.argv:
-            args.warmup = 3
+            args.warmup = 10
         result = decode_workload(args)
     elif args.workload == "gemm_bf16_32x24_131072x16384x64":
         if "--steps" not in sys.argv:
@@ -1075,6 +1087,16 @@ def main():
         result = gd_workload(args)
     else:
         result = gemv_workload(args)
+        if args.workload == "gemv16x12_65536x8192" and not args.no_lo_plane:
+            # The same products with a bfloat16 lo parity plane (6-byte parity elements).
+            import copy
+            largs = copy.copy(args)
+            largs.workload, largs.no_cpu_baseline = "gemv16x12_bf16lo_65536x8192", True
+            torch.cuda.empty_cache()
+            lo = gemv_workload(largs)
+            result["bf16_lo_plane"] = {key: lo[key] for key in ("value", "unit", "steps", "warmup", "ms_per_step",
+                                                                "config", "gemv_ms_mean", "decode_ms_mean",
+                                                                "roofline")}
         if args.workload == "gemv16x12_65536x8192" and not args.no_dense:
             # The metric's GEMM half: the dense bf16 workload in the same run, 20 timed calls.
             import copy

@@ -300,22 +300,37 @@ __device__ inline void load_pe(const YT* p, YT (&v)[PE]) {
     }
 }
 
-// One workgroup per (set, chunk): after the elimination its four waves copy
-// the systematic survivors, then combine the missing blocks on the fp64
-// matrix cores (the combination is bound by their issue rate; the copy by
-// HBM writes).
-// KS: matrix-core K steps (4 survivors each) the kernel is built for, k <= 4 KS.
-template <int KS, int E, typename YT>
+// SIMD of the calling wave within its compute unit (hardware register
+// HW_ID, bits 5:4).  The four waves of a 256-thread workgroup run on four
+// different SIMDs.
+__device__ inline int simd_id() {
+    return static_cast<int>(__builtin_amdgcn_s_getreg(4 | (4 << 6) | ((2 - 1) << 11)) & 3);
+}
+
+// One workgroup per (set, chunk).
+// E == 4: the wave on SIMD 0 of its compute unit (wave 0 if none is) forms
+// D and then copies the systematic survivors; the other three waves combine
+// the missing blocks on the fp64 matrix cores.  Vector instructions do not
+// overlap with fp64 matrix instructions on the same SIMD, so every compute
+// unit keeps the copies and the elimination on one SIMD and the matrix work
+// on the other three.  Which wave takes which role changes only the timing.
+// E == 1: wave 0 eliminates while the others start copying; then all four
+// combine.
+// KS: matrix-core K steps (4 survivors each) the kernel is built for, k <= 4 KS;
+// FULL: k == 4 KS (no padding steps).
+template <int KS, int E, typename YT, bool FULL>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
                                                                int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
     __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 256 * kDecodePE : 1];   // per-wave output tile
+    __shared__ int32_t sSimd[kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int k = a.k;
     const int64_t b = blockIdx.x / chunks;
     const int64_t chunk = blockIdx.x % chunks;
     const bool writer = (chunk == 0 && tid == 0);
+    if (lane == 0) sSimd[wv] = simd_id();             // read after setup_set's barriers
     if (!setup_set<kThreads>(a, single, b, writer, sm)) return;
     const int m = sm.m;
     const int first_par = k - m;
@@ -355,7 +370,13 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         }
     }
 
-    if (m > 0 && wv == 0) eliminate_set(a, sm, m, first_par, lane, sD);
+    // the eliminating wave (E == 4: also the copying wave)
+    int ew = 0;
+    if constexpr (E == 4) {
+#pragma unroll
+        for (int w = kWaves - 1; w >= 0; --w) ew = sSimd[w] == 0 ? w : ew;
+    }
+    if (m > 0 && wv == ew) eliminate_set(a, sm, m, first_par, lane, sD);
     __syncthreads();
     if (sm.status != 0) {
         if (writer) a.info[b] = sm.status;
@@ -382,23 +403,34 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         }
     }
 
-    // E == 4: U survivors' loads in flight per thread (straight-line: a batch
-    // past the last survivor re-reads the last one and stores nothing).
-    constexpr int U = 8;
-    for (int e = e0 + E * tid; E == 4 && e < e1; e += E * kThreads) {
-        const int t = e / s, col = e - t * s;
-        const int64_t orow = static_cast<int64_t>(t) * a.ldo + col;
-        for (int c0 = 0; c0 < first_par; c0 += U) {
-            float v[U][E];
+    // E == 4: the copying wave takes the systematic survivors block by block,
+    // U four-element items per lane in flight (a batch past the block's end
+    // re-reads its last item and stores nothing).  With dense output rows
+    // (ldo == s) element e of a block is at offset e from its first row.
+    if constexpr (E == 4) {
+        if (wv == ew) {
+            constexpr int U = 4;
+            const bool dense = a.ldo == a.s;
+            for (int c = 0; c < first_par; ++c) {
+                const int w = sm.S[c];
+                const YT* yr = Y + sm.yoff[c];
+                float* ob = out + sm.ooff[w];
+                const int elim = min(e1, sm.lim[w] * s);    // the block's elements inside A
+                for (int e = e0 + 4 * lane; e < elim; e += 256 * U) {
+                    float v[U][4];
 #pragma unroll
-            for (int u = 0; u < U; ++u) load_f32<E, YT>(Y + sm.yoff[min(c0 + u, first_par - 1)] + e, v[u]);
+                    for (int u = 0; u < U; ++u) load_f32<4, YT>(yr + min(e + 256 * u, elim - 4), v[u]);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (c0 + u < first_par) {
-                    const int w = sm.S[c0 + u];
-                    if (t < sm.lim[w]) store_out<E>(a, out, sm.ooff[w] + orow, v[u]);
+                    for (int u = 0; u < U; ++u) {
+                        const int ee = e + 256 * u;
+                        if (ee < elim) {
+                            const int64_t off = dense ? ee : static_cast<int64_t>(ee / s) * a.ldo + ee % s;
+                            store_out<4>(a, ob, off, v[u]);
+                        }
+                    }
                 }
             }
+            return;
         }
     }
     if (m == 0) return;
@@ -429,7 +461,8 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         constexpr int W = 16 * PE;
         double* buf = sOut[wv];
         const int ngroups = (e1 - e0 + W - 1) / W;
-        for (int gp = wv; gp < ngroups; gp += kWaves) {
+        const int crank = wv < ew ? wv : wv - 1;        // rank among the three combining waves
+        for (int gp = crank; gp < ngroups; gp += kWaves - 1) {
             const int base = e0 + gp * W;
             // a group past the chunk's end reads the block's last PE elements
             // instead (in bounds; those columns are not stored)
@@ -443,7 +476,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
 #pragma unroll
             for (int st = 0; st < KS; ++st) {
                 // padding steps (k not a multiple of 4) contribute exact zeros
-                const bool ok = (valid >> st) & 1u;
+                const bool ok = FULL || ((valid >> st) & 1u);
 #pragma unroll
                 for (int q = 0; q < PE; ++q)
                     acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], ok ? static_cast<double>(yv[st][q]) : 0.0,
@@ -454,16 +487,22 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
             for (int v = 0; v < 4; ++v)
 #pragma unroll
                 for (int q = 0; q < PE; ++q) buf[(4 * v + lk) * W + PE * li + q] = acc[q][v];
+            // each store instruction covers 16 / PE blocks, 4 PE lanes (W
+            // elements, whole 128-byte lines for PE = 2) per block
+            constexpr int QPB = 4 * PE;
 #pragma unroll
             for (int h = 0; h < PE; ++h) {
-                const int bb = lane >> 2, g4 = (lane & 3) + 4 * h, eg = base + 4 * g4;
+                const int bb = lane / QPB + (16 / PE) * h, g4 = lane % QPB, eg = base + 4 * g4;
                 if (bb < m && eg < e1) {
                     double v4[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) v4[i] = buf[bb * W + 4 * g4 + i];
-                    const int t = eg / s, col = eg - t * s;     // s % 4 == 0: the four share row t
+                    // s % 4 == 0: the four share one row; dense rows (ldo == s) need no division
                     const int w = sm.miss[bb];
-                    if (t < sm.lim[w]) store_out<4>(a, out, sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col, v4);
+                    if (eg < sm.lim[w] * s) {
+                        const int64_t off = a.ldo == a.s ? eg : static_cast<int64_t>(eg / s) * a.ldo + eg % s;
+                        store_out<4>(a, out, sm.ooff[w] + off, v4);
+                    }
                 }
             }
         }
@@ -481,7 +520,7 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
             f64x4v acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int st = 0; st < KS; ++st) {
-                const double bv = (valid >> st) & 1u ? static_cast<double>(yv[st]) : 0.0;
+                const double bv = (FULL || ((valid >> st) & 1u)) ? static_cast<double>(yv[st]) : 0.0;
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], bv, acc, 0, 0, 0);
             }
             if (e < e1) {
@@ -521,20 +560,28 @@ hipError_t launch_fast(const DecodeArgs& a, const DecodeSet& single, hipStream_t
     const int ksteps = (a.k + 3) / 4;
     const dim3 grid(static_cast<unsigned>(blocks));
     const int per32 = static_cast<int>(per);
-#define CODED_FAST(KS)                                                                                      \
-    do {                                                                                                    \
-        if (a.y_f64)                                                                                        \
-            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, double>), grid, dim3(kThreads), 0, st, a, single, \
-                               chunks, per32);                                                              \
-        else                                                                                                \
-            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, float>), grid, dim3(kThreads), 0, st, a, single,  \
-                               chunks, per32);                                                              \
+#define CODED_FAST_F(KS, FULL)                                                                                \
+    do {                                                                                                      \
+        if (a.y_f64)                                                                                          \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, double, FULL>), grid, dim3(kThreads), 0, st, a,     \
+                               single, chunks, per32);                                                        \
+        else                                                                                                  \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, float, FULL>), grid, dim3(kThreads), 0, st, a,      \
+                               single, chunks, per32);                                                        \
+    } while (0)
+#define CODED_FAST(KS)                          \
+    do {                                        \
+        if (a.k == 4 * (KS))                    \
+            CODED_FAST_F(KS, true);             \
+        else                                    \
+            CODED_FAST_F(KS, false);            \
     } while (0)
     if (ksteps <= 4) CODED_FAST(4);
     else if (ksteps <= 8) CODED_FAST(8);
     else if (ksteps <= 12) CODED_FAST(12);
     else CODED_FAST(16);
 #undef CODED_FAST
+#undef CODED_FAST_F
     return hipGetLastError();
 }
 

@@ -98,8 +98,9 @@ __device__ inline double lane_value(double v, int lane) {
 // D[b][c] = sD[c * kFastLd + b] for b < kFastM (rows >= m zero); on a zero
 // pivot sm.status = first_par + j + 1.  The operations on rows < m do not
 // depend on MM, so every MM >= m gives the same D.
-template <int MM>
-__device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm, int m, int first_par, int lane, double* sD) {
+// Meta: any bookkeeping with S (sorted survivors), miss and status as in SetMeta.
+template <int MM, typename Meta>
+__device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, Meta& sm, int m, int first_par, int lane, double* sD) {
     static_assert(MM <= kFastM, "MM");
     const int k = a.k;
     const int c = lane - m;
@@ -175,12 +176,15 @@ __device__ __forceinline__ void eliminate_wave(const DecodeArgs& a, SetMeta& sm,
 }
 
 // The smallest register size that holds a set with m missing blocks.
-__device__ __forceinline__ void eliminate_set(const DecodeArgs& a, SetMeta& sm, int m, int first_par, int lane,
+template <typename Meta>
+__device__ __forceinline__ void eliminate_set(const DecodeArgs& a, Meta& sm, int m, int first_par, int lane,
                                               double* sD) {
     if (m <= 4)
         eliminate_wave<4>(a, sm, m, first_par, lane, sD);
     else if (m <= 8)
         eliminate_wave<8>(a, sm, m, first_par, lane, sD);
+    else if (m <= 12)
+        eliminate_wave<12>(a, sm, m, first_par, lane, sD);
     else
         eliminate_wave<kFastM>(a, sm, m, first_par, lane, sD);
 }

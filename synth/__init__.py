@@ -7,8 +7,8 @@ path take their inputs from here.
 """
 from .inputs import (  # noqa: F401
     STREAM_A, STREAM_X, STREAM_P, STREAM_RUNTIME, STREAM_NOISE, STREAM_WSTAR,
-    STREAM_PT, ROW_CHUNK, generator, gaussian, gaussian_rows, integers,
+    STREAM_PT, STREAM_SETS, ROW_CHUNK, generator, gaussian, gaussian_rows, integers,
     bf16_round, bf16_bits, bf16_from_bits, parity_matrix, integer_parity_matrix,
-    worst_decode_condition, conditioned_parity_matrix,
+    worst_decode_condition, conditioned_parity_matrix, exact_parity_sets,
 )
 from .workloads import WORKLOADS, Workload, gd_codes  # noqa: F401

@@ -20,6 +20,7 @@ STREAM_RUNTIME = 4  # worker runtimes (consumed by the counter-based SplitMix64,
 STREAM_NOISE = 5    # label noise of the least-squares workload
 STREAM_WSTAR = 6    # ground-truth weights of the least-squares workload
 STREAM_PT = 7       # parity rows of the second code (the one applied to A^T)
+STREAM_SETS = 10    # survivor sets with a fixed number of parity survivors
 
 ROW_CHUNK = 4096    # rows per independently seeded chunk of a large matrix
 
@@ -158,3 +159,21 @@ def conditioned_parity_matrix(n: int, k: int, seed: int, candidates: int, stream
             best = (P, c, w)
     return best
 
+
+
+def exact_parity_sets(n: int, k: int, m: int, batch: int, seed: int) -> np.ndarray:
+    """batch x k int32 survivor sets, each with exactly m parity workers (of
+    k..n-1) and k - m systematic ones (of 0..k-1), drawn uniformly and
+    independently (repeats allowed), each row in a random order.  Inputs for
+    measuring the decode's cost against the number of missing blocks."""
+    if not (0 <= m <= min(k, n - k)):
+        raise ValueError("need 0 <= m <= min(k, n - k)")
+    g = generator(seed, STREAM_SETS, m)
+    out = np.empty((batch, k), dtype=np.int32)
+    for b in range(batch):
+        sys_ = g.choice(k, size=k - m, replace=False)
+        par = k + g.choice(n - k, size=m, replace=False)
+        row = np.concatenate([sys_, par]).astype(np.int32)
+        g.shuffle(row)
+        out[b] = row
+    return out
