@@ -28,6 +28,15 @@
 // one chunk.  Rows past the block read a clamped row; padding rows (past q)
 // are written as zero in the epilogue.
 //
+// With buffer addressing (BUF, used when every offset fits in 31 bits) each
+// load is one per-thread offset, fixed for the whole K loop, from one base per
+// operand, plus the chunk's byte offset in a scalar register: no vector
+// instruction is spent on addresses, and the prefetches past the last chunk
+// get an offset beyond the buffer's size, which the hardware answers with
+// zeros and no memory access.  Vector instructions do not overlap with the
+// fp64 matrix instructions on a SIMD, so every one removed from the K loop
+// shortens it.
+//
 // The four waves take quarters of each chunk's K range and keep partial sums
 // of the whole tile; the partials are added through LDS in a fixed order.
 //
@@ -77,7 +86,15 @@ __device__ inline f32x4m load_stream4(const float* p) {
     return __builtin_nontemporal_load(reinterpret_cast<const f32x4m*>(p));
 }
 
-template <int RT, int NCT, bool NARROW, int KC, int PF>
+// Raw buffer resource over `bytes` bytes from `base` (no stride, no format:
+// the gfx9 dword-3 value); loads at offsets >= bytes return zeros.
+__device__ inline __amdgpu_buffer_rsrc_t raw_buffer(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), static_cast<int>(bytes),
+                                             0x00020000);
+}
+constexpr int kAuxNonTemporal = 2;   // cache-policy bits of the load: nt
+
+template <int RT, int NCT, bool NARROW, int KC, int PF, bool BUF>
 __global__ __launch_bounds__(kMmThreads) void gemm_f32_mfma_kernel(WorkerArgs a, int64_t stiles, int64_t ptiles,
                                                                    int64_t c0) {
     using C = MmCfg<RT, NCT, NARROW, KC>;
@@ -136,17 +153,63 @@ __global__ __launch_bounds__(kMmThreads) void gemm_f32_mfma_kernel(WorkerArgs a,
     const float* X = static_cast<const float*>(a.X);
     const float* gx[C::kXLoads];
     int ofs_x[C::kXLoads], xk[C::kXLoads];
+    uint32_t xoff[C::kXLoads];
 #pragma unroll
     for (int i = 0; i < C::kXLoads; ++i) {
         const int e = tid + kMmThreads * i;
         const int kk = e / C::kSP, cc = e % C::kSP;
         xk[i] = kk;
         ofs_x[i] = cc * C::kXStride + kk;
-        gx[i] = X + (c0 + cc < a.s ? c0 + cc : a.s - 1);   // absent columns read a real one, never stored
+        const int64_t col = c0 + cc < a.s ? c0 + cc : a.s - 1;   // absent columns read a real one, never stored
+        gx[i] = X + col;
+        xoff[i] = static_cast<uint32_t>((static_cast<int64_t>(kk) * a.ldx + col) * 4);
     }
+
+    // Buffer addressing: the operands' buffers and this thread's byte offsets
+    // (a systematic block's rows past q read as zeros; padding rows are
+    // stored as zeros in the epilogue).
+    const float* abase;
+    int64_t rows_in, rstride;
+    uint32_t abytes;
+    if (parity) {
+        abase = static_cast<const float*>(a.parity) + static_cast<int64_t>(worker - a.k) * a.qb * a.r;
+        rows_in = a.qb;
+        rstride = a.r;
+        abytes = static_cast<uint32_t>(((a.planes == 2 ? plane_elems : 0) + a.qb * a.r) * 4);
+    } else {
+        abase = static_cast<const float*>(a.A) + static_cast<int64_t>(worker) * a.qb * a.lda;
+        rows_in = a.q - static_cast<int64_t>(worker) * a.qb;
+        rows_in = rows_in < a.qb ? rows_in : a.qb;
+        rstride = a.lda;
+        abytes = static_cast<uint32_t>((rows_in > 0 ? rows_in : 0) * a.lda * 4);
+    }
+    uint32_t aoff[C::kALoads];
+#pragma unroll
+    for (int p = 0; p < C::kALoads; ++p) {
+        const int rho = (tid + kMmThreads * p) / (KC / 4);
+        int64_t t = t0 + rho % hrows;
+        t = t < rows_in ? t : rows_in - 1;
+        t = t > 0 ? t : 0;
+        aoff[p] = static_cast<uint32_t>(((parity ? (rho / hrows) * plane_elems : 0) + t * rstride + acol[p]) * 4);
+    }
+    const uint32_t xbytes = static_cast<uint32_t>(a.r * a.ldx * 4);
+    const __amdgpu_buffer_rsrc_t rsA = raw_buffer(abase, abytes);
+    const __amdgpu_buffer_rsrc_t rsX = raw_buffer(X, xbytes);
 
     auto load_chunk = [&](int c, f32x4m* R, float* XR) {
         const bool live = c < nch;
+        if constexpr (BUF) {
+            // scalar chunk offsets; past the last chunk, offsets beyond the buffers
+            const uint32_t sa = live ? static_cast<uint32_t>(c) * KC * 4 : abytes;
+            const uint32_t sx = live ? static_cast<uint32_t>(c) * KC * static_cast<uint32_t>(a.ldx) * 4 : xbytes;
+#pragma unroll
+            for (int p = 0; p < C::kALoads; ++p)
+                R[p] = __builtin_bit_cast(f32x4m, __builtin_amdgcn_raw_buffer_load_b128(rsA, aoff[p], sa, kAuxNonTemporal));
+#pragma unroll
+            for (int i = 0; i < C::kXLoads; ++i)
+                XR[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, xoff[i], sx, 0));
+            return;
+        }
 #pragma unroll
         for (int p = 0; p < C::kALoads; ++p) {
             int kk = c * KC + acol[p];
@@ -164,6 +227,13 @@ __global__ __launch_bounds__(kMmThreads) void gemm_f32_mfma_kernel(WorkerArgs a,
     auto store_chunk = [&](int buf, int kvalid, const f32x4m* R, const float* XR) {
         float* Ab = As + buf * C::kRows * C::kStride;
         double* Xb = Xs + buf * C::kSP * C::kXStride;
+        if (BUF && kvalid >= KC) {     // a whole chunk: nothing to zero
+#pragma unroll
+            for (int p = 0; p < C::kALoads; ++p) *reinterpret_cast<f32x4m*>(Ab + ofs_a[p]) = R[p];
+#pragma unroll
+            for (int i = 0; i < C::kXLoads; ++i) Xb[ofs_x[i]] = static_cast<double>(XR[i]);
+            return;
+        }
 #pragma unroll
         for (int p = 0; p < C::kALoads; ++p)
             *reinterpret_cast<f32x4m*>(Ab + ofs_a[p]) = acol[p] < kvalid ? R[p] : f32x4m{0.f, 0.f, 0.f, 0.f};
@@ -274,6 +344,16 @@ __global__ __launch_bounds__(kMmThreads) void gemm_f32_mfma_kernel(WorkerArgs a,
     }
 }
 
+// Buffer addressing needs every byte offset (and the past-the-end offsets,
+// which equal a buffer's size) below 2^31.
+bool buffer_offsets_fit(const WorkerArgs& a) {
+    const int64_t lim = (int64_t(1) << 31) - 1;
+    const int64_t sys = a.qb * a.lda * 4;
+    const int64_t par = ((a.planes == 2 ? static_cast<int64_t>(a.n - a.k) * a.qb * a.r : 0) + a.qb * a.r) * 4;
+    const int64_t x = a.r * a.ldx * 4 + a.s * 4;
+    return sys < lim && par < lim && x < lim;
+}
+
 template <int RT, int NCT, bool NARROW, int KC, int PF>
 hipError_t launch_mm(const WorkerArgs& a, int64_t c0, hipStream_t st) {
     using C = MmCfg<RT, NCT, NARROW, KC>;
@@ -282,8 +362,12 @@ hipError_t launch_mm(const WorkerArgs& a, int64_t c0, hipStream_t st) {
     const int64_t blocks = stiles * a.n_sys + ptiles * a.n_par;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((gemm_f32_mfma_kernel<RT, NCT, NARROW, KC, PF>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(kMmThreads), 0, st, a, stiles, ptiles, c0);
+    if (buffer_offsets_fit(a))
+        hipLaunchKernelGGL((gemm_f32_mfma_kernel<RT, NCT, NARROW, KC, PF, true>), dim3(static_cast<unsigned>(blocks)),
+                           dim3(kMmThreads), 0, st, a, stiles, ptiles, c0);
+    else
+        hipLaunchKernelGGL((gemm_f32_mfma_kernel<RT, NCT, NARROW, KC, PF, false>),
+                           dim3(static_cast<unsigned>(blocks)), dim3(kMmThreads), 0, st, a, stiles, ptiles, c0);
     return hipGetLastError();
 }
 
