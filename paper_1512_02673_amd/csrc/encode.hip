@@ -4,9 +4,10 @@
 //
 // The contraction has k (<= a few dozen) terms per output element and the
 // whole pass streams A once and writes the parity planes once, so it is bound
-// by HBM bandwidth, not arithmetic: each thread owns a short vector of
-// columns of one block row t, walks the k blocks j, and keeps up to
-// kGroup parity accumulators in registers.  Parity rows beyond kGroup are
+// by HBM bandwidth, not arithmetic (about 2 flops per byte, far below the
+// matrix cores' ridge): each thread owns a short vector of columns of one
+// block row t, walks the k blocks j with kBatch loads in flight, and keeps up
+// to kGroup parity accumulators in registers; the sum runs over j in order.  Parity rows beyond kGroup are
 // handled by further groups (grid.y), each re-reading A.
 //
 // Storage: with planes == 2 the exact sum (fp64 for fp32 inputs, fp32 for
@@ -18,6 +19,7 @@ namespace {
 
 constexpr int kGroup = 8;       // parity rows per pass
 constexpr int kThreads = 256;
+constexpr int kBatch = 8;       // blocks whose loads are in flight together
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
     uint32_t b = __float_as_uint(f);
@@ -52,24 +54,33 @@ __global__ __launch_bounds__(kThreads) void encode_f32_kernel(EncodeArgs a, int6
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[p][v] = 0.0;
 
-    for (int j = 0; j < k; ++j) {
-        const int64_t row = j * a.qb + t;
-        if (row >= a.q) break;               // zero padding: contributes nothing
-        float v4[VEC];
-        const float* src = A + row * a.lda + c;
-        if constexpr (VEC == 4) {
-            const float4 f = *reinterpret_cast<const float4*>(src);
-            v4[0] = f.x; v4[1] = f.y; v4[2] = f.z; v4[3] = f.w;
-        } else {
+    // Blocks whose row t lies inside A (rows of later blocks are the zero
+    // padding and contribute nothing); their loads go out kBatch at a time.
+    const int kv = static_cast<int>(min<int64_t>(k, (a.q - t + a.qb - 1) / a.qb));
+    for (int j0 = 0; j0 < kv; j0 += kBatch) {
+        float v4[kBatch][VEC];
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) v4[v] = src[v];
+        for (int u = 0; u < kBatch; ++u) {
+            const int j = min(j0 + u, kv - 1);   // past the last block: re-read it, not used
+            const float* src = A + (static_cast<int64_t>(j) * a.qb + t) * a.lda + c;
+            if constexpr (VEC == 4) {
+                const float4 f = *reinterpret_cast<const float4*>(src);
+                v4[u][0] = f.x; v4[u][1] = f.y; v4[u][2] = f.z; v4[u][3] = f.w;
+            } else {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) v4[u][v] = src[v];
+            }
         }
 #pragma unroll
-        for (int p = 0; p < kGroup; ++p) {
-            if (p < np) {
-                const double g = sP[p * k + j];
+        for (int u = 0; u < kBatch; ++u) {
+            if (j0 + u >= kv) break;
 #pragma unroll
-                for (int v = 0; v < VEC; ++v) acc[p][v] = fma(g, static_cast<double>(v4[v]), acc[p][v]);
+            for (int p = 0; p < kGroup; ++p) {
+                if (p < np) {
+                    const double g = sP[p * k + j0 + u];
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) acc[p][v] = fma(g, static_cast<double>(v4[u][v]), acc[p][v]);
+                }
             }
         }
     }
@@ -142,29 +153,36 @@ __global__ __launch_bounds__(kThreads) void encode_bf16_kernel(EncodeArgs a, int
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[p][v] = 0.0f;
 
-    for (int j = 0; j < k; ++j) {
-        const int64_t row = j * a.qb + t;
-        if (row >= a.q) break;
-        float v8[VEC];
-        const uint16_t* src = A + row * a.lda + c;
-        if constexpr (VEC == 8) {
-            const uint4 u = *reinterpret_cast<const uint4*>(src);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    const int kv = static_cast<int>(min<int64_t>(k, (a.q - t + a.qb - 1) / a.qb));   // blocks with row t inside A
+    for (int j0 = 0; j0 < kv; j0 += kBatch) {
+        float v8[kBatch][VEC];
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                v8[2 * h] = __uint_as_float(w[h] << 16);
-                v8[2 * h + 1] = __uint_as_float(w[h] & 0xFFFF0000u);
+        for (int u = 0; u < kBatch; ++u) {
+            const int j = min(j0 + u, kv - 1);   // past the last block: re-read it, not used
+            const uint16_t* src = A + (static_cast<int64_t>(j) * a.qb + t) * a.lda + c;
+            if constexpr (VEC == 8) {
+                const uint4 q4 = *reinterpret_cast<const uint4*>(src);
+                const uint32_t w[4] = {q4.x, q4.y, q4.z, q4.w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    v8[u][2 * h] = __uint_as_float(w[h] << 16);
+                    v8[u][2 * h + 1] = __uint_as_float(w[h] & 0xFFFF0000u);
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) v8[u][v] = bf16_to_f32(src[v]);
             }
-        } else {
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) v8[v] = bf16_to_f32(src[v]);
         }
 #pragma unroll
-        for (int p = 0; p < kGroup; ++p) {
-            if (p < np) {
-                const float g = sP[p * k + j];
+        for (int u = 0; u < kBatch; ++u) {
+            if (j0 + u >= kv) break;
 #pragma unroll
-                for (int v = 0; v < VEC; ++v) acc[p][v] = fmaf(g, v8[v], acc[p][v]);
+            for (int p = 0; p < kGroup; ++p) {
+                if (p < np) {
+                    const float g = sP[p * k + j0 + u];
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) acc[p][v] = fmaf(g, v8[u][v], acc[p][v]);
+                }
             }
         }
     }
