@@ -33,11 +33,20 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+# Kernels that accumulate on the matrix cores in loops: keep the accumulators
+# in vector registers (otherwise the compiler copies them to and from the
+# accumulation registers around loop iterations, vector instructions that do
+# not overlap with the fp64 matrix work; the fp32 products at s = 16..64
+# measured 5% faster, the others unchanged).
+MFMA_VGPR_FORM = {"worker_f32_mfma.hip", "decode.hip", "worker_bf16.hip"}
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, src + ".o")
     path = os.path.join(CSRC, src)
     if src.endswith(".hip"):
-        cmd = [hipcc(), "-x", "hip", *DEVICE, *COMMON, "-c", path, "-o", obj]
+        extra = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"] if src in MFMA_VGPR_FORM else []
+        cmd = [hipcc(), "-x", "hip", *DEVICE, *extra, *COMMON, "-c", path, "-o", obj]
     else:
         cmd = [hipcc(), *COMMON, "-D__HIP_PLATFORM_AMD__", "-c", path, "-o", obj]
     if verbose:

@@ -575,3 +575,37 @@ def test_conditioned_gd_codes_single_plane_every_survivor_set(lib, torch, which)
     assert worst["conditioned"] <= TOL_F32, worst
     if "plain" in worst:
         assert worst["plain"] > TOL_F32, worst
+
+
+@pytest.mark.parametrize("n,k", [(64, 48), (20, 13)])
+@pytest.mark.parametrize("s,pad", [(8, 0), (8, 4), (4, 2), (12, 0)])
+def test_decode_matrix_core_path_roles_and_strided_out(lib, torch, n, k, s, pad):
+    """The matrix-core decode with four-element vectors (s a multiple of 4): the
+    copying wave and the three combining waves, dense rows (ldo == s) and padded
+    rows, k a multiple of 4 (no padding steps) or not, sets with 0 to min(k, n-k)
+    missing blocks; against the oracle and bit for bit against single decodes."""
+    q, r = 1000, 24
+    P, A, X = make_inputs(n, k, q, r, s, 21)
+    G = oc.systematic_generator(P)
+    Y = oc.worker_products(oc.encode(G, oc.pad_and_split(A, k)), X)
+    code = lib.Code(n, k, G, 2)
+    dY = torch.from_numpy(Y).to("cuda")
+    mmax = min(k, n - k)
+    sets = np.concatenate([synth.exact_parity_sets(n, k, m, 2, 5) for m in sorted({0, 1, 3, mmax // 2, mmax})])
+    base = torch.full((len(sets), q, s + pad), float("nan"), dtype=torch.float32, device="cuda")
+    out = base[:, :, :s]
+    info = info_tensor(torch, len(sets))
+    lib.coded_decode_batched(code, torch.from_numpy(sets).cuda(), dY, q, out, info)
+    torch.cuda.synchronize()
+    assert np.all(info.cpu().numpy() == 0)
+    got_all = base.cpu().numpy()
+    for bi, S in enumerate(sets):
+        ref = oc.decode_from_all(G, S, Y, q)
+        tol = 2.0 ** -23 + 1e-14 * np.linalg.cond(G[np.sort(S)]) * k
+        assert normwise_rel_err(got_all[bi, :, :s], ref) <= tol, bi
+        if pad:
+            assert np.all(np.isnan(got_all[bi, :, s:]))
+        single = torch.full((q, s + pad), float("nan"), dtype=torch.float32, device="cuda")
+        lib.coded_decode(code, S, dY, q, single[:, :s], info[:1])
+        torch.cuda.synchronize()
+        assert np.array_equal(single.cpu().numpy()[:, :s], got_all[bi, :, :s]), bi
