@@ -318,7 +318,17 @@ __device__ inline int simd_id() {
 // combine.
 // KS: matrix-core K steps (4 survivors each) the kernel is built for, k <= 4 KS;
 // FULL: k == 4 KS (no padding steps).
-template <int KS, int E, typename YT, bool FULL>
+// Raw buffer over `bytes` bytes (gfx9 dword-3 value: no stride, no format).
+__device__ inline __amdgpu_buffer_rsrc_t y_buffer(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), static_cast<int>(bytes),
+                                             0x00020000);
+}
+
+// YBUF (E == 4, Y's byte offsets below 2^31): the combining waves read Y as a
+// raw buffer, each lane's offset per survivor fixed for the set and the
+// group's offset in a scalar register, so the loads need no vector address
+// arithmetic.
+template <int KS, int E, typename YT, bool FULL, bool YBUF>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
                                                                int elems_per_block) {
     __shared__ SetMeta sm;
@@ -461,15 +471,57 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         constexpr int W = 16 * PE;
         double* buf = sOut[wv];
         const int ngroups = (e1 - e0 + W - 1) / W;
-        const int crank = wv < ew ? wv : wv - 1;        // rank among the three combining waves
+        const int crank = __builtin_amdgcn_readfirstlane(wv < ew ? wv : wv - 1);   // rank among the combining waves
+        // each store instruction covers 16 / PE blocks, 4 PE lanes (W
+        // elements, whole 128-byte lines for PE = 2) per block; this lane's
+        // block, its first row in out and its element limit are fixed for the set
+        constexpr int QPB = 4 * PE;
+        const int g4 = lane % QPB;
+        float* obase[PE];
+        int elim[PE];
+#pragma unroll
+        for (int h = 0; h < PE; ++h) {
+            const int bb = lane / QPB + (16 / PE) * h;
+            const int w = sm.miss[bb < m ? bb : 0];
+            obase[h] = out + sm.ooff[w];
+            elim[h] = bb < m ? min(e1, sm.lim[w] * s) : 0;   // 0: no block for this lane
+        }
+        const bool dense = a.ldo == a.s;
+        // YBUF: byte offset of this lane's elements of survivor 4 st + lk (a
+        // group's elements past the block's end read the next result or zeros
+        // past the buffer; those columns are not stored)
+        uint32_t yb[YBUF ? KS : 1];
+        const __amdgpu_buffer_rsrc_t yrs =
+            y_buffer(Y, static_cast<uint32_t>(YBUF ? static_cast<int64_t>(a.n) * total * sizeof(YT) : 0));
+        if constexpr (YBUF) {
+#pragma unroll
+            for (int st = 0; st < KS; ++st) yb[st] = static_cast<uint32_t>((yo[st] + PE * li) * sizeof(YT));
+        }
         for (int gp = crank; gp < ngroups; gp += kWaves - 1) {
             const int base = e0 + gp * W;
-            // a group past the chunk's end reads the block's last PE elements
-            // instead (in bounds; those columns are not stored)
-            const int el = min(base + PE * li, total - PE);
             YT yv[KS][PE];
+            if constexpr (YBUF) {
+                static_assert(PE == 2, "one 2-element load per survivor");
+                const uint32_t so = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(base) * sizeof(YT));
 #pragma unroll
-            for (int st = 0; st < KS; ++st) load_pe<PE>(Y + yo[st] + el, yv[st]);
+                for (int st = 0; st < KS; ++st) {
+                    if constexpr (sizeof(YT) == 8) {
+                        const double2 d = __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(yrs, yb[st], so, 0));
+                        yv[st][0] = d.x;
+                        yv[st][1] = d.y;
+                    } else {
+                        const float2 f = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(yrs, yb[st], so, 0));
+                        yv[st][0] = f.x;
+                        yv[st][1] = f.y;
+                    }
+                }
+            } else {
+                // a group past the chunk's end reads the block's last PE elements
+                // instead (in bounds; those columns are not stored)
+                const int el = min(base + PE * li, total - PE);
+#pragma unroll
+                for (int st = 0; st < KS; ++st) load_pe<PE>(Y + yo[st] + el, yv[st]);
+            }
             f64x4v acc[PE];
 #pragma unroll
             for (int q = 0; q < PE; ++q) acc[q] = f64x4v{0.0, 0.0, 0.0, 0.0};
@@ -482,27 +534,25 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
                     acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[st], ok ? static_cast<double>(yv[st][q]) : 0.0,
                                                                   acc[q], 0, 0, 0);
             }
-            // item v of lane (li, lk): block 4 v + lk, element PE li + q of acc[q]
+            // item v of lane (li, lk): block 4 v + lk, element PE li + q of acc[q],
+            // kept in the tile at [block][q][li] (one 8-byte write per item, no
+            // register moves)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
 #pragma unroll
-                for (int q = 0; q < PE; ++q) buf[(4 * v + lk) * W + PE * li + q] = acc[q][v];
-            // each store instruction covers 16 / PE blocks, 4 PE lanes (W
-            // elements, whole 128-byte lines for PE = 2) per block
-            constexpr int QPB = 4 * PE;
+                for (int q = 0; q < PE; ++q) buf[(4 * v + lk) * W + 16 * q + li] = acc[q][v];
 #pragma unroll
             for (int h = 0; h < PE; ++h) {
-                const int bb = lane / QPB + (16 / PE) * h, g4 = lane % QPB, eg = base + 4 * g4;
-                if (bb < m && eg < e1) {
-                    double v4[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) v4[i] = buf[bb * W + 4 * g4 + i];
+                const int bb = lane / QPB + (16 / PE) * h, eg = base + 4 * g4;
+                if (eg < elim[h]) {
+                    // elements 4 g4 .. 4 g4 + 3: (li, q) = (2 g4, 0), (2 g4, 1), (2 g4 + 1, 0), (2 g4 + 1, 1)
+                    static_assert(PE == 2, "tile order");
+                    const double2 r0 = *reinterpret_cast<const double2*>(&buf[bb * W + 2 * g4]);
+                    const double2 r1 = *reinterpret_cast<const double2*>(&buf[bb * W + 16 + 2 * g4]);
+                    const double v4[4] = {r0.x, r1.x, r0.y, r1.y};
                     // s % 4 == 0: the four share one row; dense rows (ldo == s) need no division
-                    const int w = sm.miss[bb];
-                    if (eg < sm.lim[w] * s) {
-                        const int64_t off = a.ldo == a.s ? eg : static_cast<int64_t>(eg / s) * a.ldo + eg % s;
-                        store_out<4>(a, out, sm.ooff[w] + off, v4);
-                    }
+                    const int64_t off = dense ? eg : static_cast<int64_t>(eg / s) * a.ldo + eg % s;
+                    store_out<4>(a, obase[h], off, v4);
                 }
             }
         }
@@ -560,14 +610,23 @@ hipError_t launch_fast(const DecodeArgs& a, const DecodeSet& single, hipStream_t
     const int ksteps = (a.k + 3) / 4;
     const dim3 grid(static_cast<unsigned>(blocks));
     const int per32 = static_cast<int>(per);
-#define CODED_FAST_F(KS, FULL)                                                                                \
-    do {                                                                                                      \
-        if (a.y_f64)                                                                                          \
-            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, double, FULL>), grid, dim3(kThreads), 0, st, a,     \
-                               single, chunks, per32);                                                        \
-        else                                                                                                  \
-            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, float, FULL>), grid, dim3(kThreads), 0, st, a,      \
-                               single, chunks, per32);                                                        \
+    // Y read as a raw buffer (E == 4) when its byte offsets fit in 31 bits
+    const bool ybuf = E == 4 && static_cast<int64_t>(a.n) * total * (a.y_f64 ? 8 : 4) < (int64_t(1) << 31);
+#define CODED_FAST_Y(KS, FULL, YB)                                                                             \
+    do {                                                                                                       \
+        if (a.y_f64)                                                                                           \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, double, FULL, YB>), grid, dim3(kThreads), 0, st, a,  \
+                               single, chunks, per32);                                                         \
+        else                                                                                                   \
+            hipLaunchKernelGGL((decode_mfma_kernel<KS, E, float, FULL, YB>), grid, dim3(kThreads), 0, st, a,   \
+                               single, chunks, per32);                                                         \
+    } while (0)
+#define CODED_FAST_F(KS, FULL)                       \
+    do {                                             \
+        if (ybuf)                                    \
+            CODED_FAST_Y(KS, FULL, E == 4);          \
+        else                                         \
+            CODED_FAST_Y(KS, FULL, false);           \
     } while (0)
 #define CODED_FAST(KS)                          \
     do {                                        \
@@ -582,6 +641,7 @@ hipError_t launch_fast(const DecodeArgs& a, const DecodeSet& single, hipStream_t
     else CODED_FAST(16);
 #undef CODED_FAST
 #undef CODED_FAST_F
+#undef CODED_FAST_Y
     return hipGetLastError();
 }
 
