@@ -515,8 +515,8 @@ def decode_workload(args):
                             f"uniform random sets with exactly {args.exact_parity} parity survivors (repeats allowed)")},
         "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
-                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double, true>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
-                     "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double, true>")},
+                     "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double, true, true>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
+                     "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double, true, true>")},
         "products": {"kernel": "gemm_f32_mfma_kernel<1, 2, true, 64, 4, true> (64 worker products, s = 8, once per run)",
                      "ms_mean": float(prod_ms.mean()), "ms_min": float(prod_ms.min()),
                      "algorithmic_bytes_per_launch": prod_bytes,
