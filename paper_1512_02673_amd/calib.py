@@ -1,7 +1,8 @@
 """Device ceilings of the GPU the library runs on (calib/ceilings.hip), the
 figures the kernels' design notes compare against besides the published
 peaks: HBM read and write bandwidth, the row-window read patterns of the
-worker kernels, and sustained matrix-instruction and fp64 vector rates."""
+worker kernels, the memory pattern of the bf16 single pass, and sustained
+matrix-instruction and fp64 vector rates."""
 from __future__ import annotations
 
 import ctypes
@@ -23,7 +24,8 @@ def lib() -> ctypes.CDLL:
         _lib.calib_write.argtypes = [p, i64, i32, i32, i32, f]
         _lib.calib_read_rows.argtypes = [p, i64, i32, i32, i32, p, f]
         _lib.calib_rate.argtypes = [i32, i32, i32, i32, p, p, f]
-        for fn in ("calib_read", "calib_write", "calib_read_rows", "calib_rate"):
+        _lib.calib_tile_pattern.argtypes = [p, p, i64, i64, i32, i32, i32, f]
+        for fn in ("calib_read", "calib_write", "calib_read_rows", "calib_rate", "calib_tile_pattern"):
             getattr(_lib, fn).restype = ctypes.c_int32
     return _lib
 
@@ -70,6 +72,18 @@ def ceilings(read_bytes: int = 3 * 2 ** 30, reps: int = 20) -> dict:
                                         ctypes.c_void_p(scratch.data_ptr())) * 1e-3) / 1e9
         for pat in range(4)}
     del buf
+    # the bf16 single pass's memory pattern at the dense workload's shape
+    q, r = 131072, 16384
+    qb = -(-q // 24)
+    A = torch.ones(q * r, dtype=torch.bfloat16, device="cuda")
+    P = torch.empty(2 * 8 * qb * r, dtype=torch.bfloat16, device="cuda")
+    moved = 2 * q * r + 4 * 8 * qb * r
+    out["single_pass_pattern_gbs"] = {
+        f"{1024 // run} rows x {run} B per wave instruction":
+            moved / (_ms(h.calib_tile_pattern, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(P.data_ptr()), q, r, run,
+                         cus, 5) * 1e-3) / 1e9
+        for run in (128, 256, 512)}
+    del A, P
     rates = {}
     kinds = [("v_mfma_f64_16x16x4f64", 0, 2000), ("v_mfma_f64_4x4x4f64", 1, 4000),
              ("v_mfma_f32_16x16x32_bf16", 2, 4000), ("v_fma_f64", 3, 20000)]

@@ -177,10 +177,10 @@ def test_code_device_buffer_is_the_callers(lib):
 
 
 def test_calibration_library_exports_its_probes():
-    """The device-ceiling probes (calib/ceilings.hip) build into their own library with four entry points."""
+    """The device-ceiling probes (calib/ceilings.hip) build into their own library with five entry points."""
     from paper_1512_02673_amd import build as _build
     if not os.path.exists(_build.CALIB_PATH):
         _build.build_calib()
     h = ctypes.CDLL(_build.CALIB_PATH)
-    for name in ("calib_read", "calib_write", "calib_read_rows", "calib_rate"):
+    for name in ("calib_read", "calib_write", "calib_read_rows", "calib_rate", "calib_tile_pattern"):
         assert hasattr(h, name), name
