@@ -181,7 +181,8 @@ __global__ __launch_bounds__(kMmThreads) void gemm_f32_mfma_kernel(WorkerArgs a,
         rows_in = a.q - static_cast<int64_t>(worker) * a.qb;
         rows_in = rows_in < a.qb ? rows_in : a.qb;
         rstride = a.lda;
-        abytes = static_cast<uint32_t>((rows_in > 0 ? rows_in : 0) * a.lda * 4);
+        // the block's rows inside A, up to the last row's r-th column
+        abytes = static_cast<uint32_t>(rows_in > 0 ? ((rows_in - 1) * a.lda + a.r) * 4 : 0);
     }
     uint32_t aoff[C::kALoads];
 #pragma unroll
