@@ -24,7 +24,7 @@ def lib() -> ctypes.CDLL:
         _lib.calib_write.argtypes = [p, i64, i32, i32, i32, f]
         _lib.calib_read_rows.argtypes = [p, i64, i32, i32, i32, p, f]
         _lib.calib_rate.argtypes = [i32, i32, i32, i32, p, p, f]
-        _lib.calib_tile_pattern.argtypes = [p, p, i64, i64, i32, i32, i32, f]
+        _lib.calib_tile_pattern.argtypes = [p, p, i64, i64, i32, i32, i32, i32, f]
         for fn in ("calib_read", "calib_write", "calib_read_rows", "calib_rate", "calib_tile_pattern"):
             getattr(_lib, fn).restype = ctypes.c_int32
     return _lib
@@ -79,10 +79,10 @@ def ceilings(read_bytes: int = 3 * 2 ** 30, reps: int = 20) -> dict:
     P = torch.empty(2 * 8 * qb * r, dtype=torch.bfloat16, device="cuda")
     moved = 2 * q * r + 4 * 8 * qb * r
     out["single_pass_pattern_gbs"] = {
-        f"{1024 // run} rows x {run} B per wave instruction":
-            moved / (_ms(h.calib_tile_pattern, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(P.data_ptr()), q, r, run,
-                         cus, 5) * 1e-3) / 1e9
-        for run in (128, 256, 512)}
+        f"reads {1024 // rr} rows x {rr} B, writes {1024 // rw} rows x {rw} B per wave instruction":
+            moved / (_ms(h.calib_tile_pattern, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(P.data_ptr()), q, r, rr,
+                         rw, cus, 5) * 1e-3) / 1e9
+        for rr, rw in ((128, 128), (256, 256), (512, 512), (512, 128))}
     del A, P
     rates = {}
     kinds = [("v_mfma_f64_16x16x4f64", 0, 2000), ("v_mfma_f64_4x4x4f64", 1, 4000),

@@ -104,22 +104,24 @@ __global__ __launch_bounds__(256) void read_rows(const float* __restrict__ A, in
 
 // The memory pattern of the bf16 single pass (encode + products) with nothing
 // else: a 512-thread workgroup per compute unit walks an equal run of units
-// (16-row tile, RUN-byte column range) of a (k = 24, n - k = 8) code, reading
-// the tile's 16 rows of all 24 blocks and writing 16 rows of each of the 16
-// parity rows (8 per plane), with the next unit's loads in flight (two
-// register sets).  Each wave instruction covers 1024 / RUN rows x RUN bytes:
-// RUN = 128 is the single pass's own pattern (64-column stages).  Rows past q
-// read the last row; rows past a block's end are not written.
+// (16-row tile, column range of RUN = max(RUNR, RUNW) bytes) of a (k = 24,
+// n - k = 8) code, reading the tile's 16 rows of all 24 blocks and writing 16
+// rows of each of the 16 parity rows (8 per plane), with the next unit's
+// loads in flight (two register sets).  A wave's load instruction covers
+// 1024 / RUNR rows x RUNR contiguous bytes, a store 1024 / RUNW rows x RUNW
+// bytes (RUN / RUNR such runs of a row are read by successive instructions).
+// Rows past q read the last row; rows past a block's end are not written.
 struct TileArgs {
     const uint16_t* A;   // q x r bf16
     uint16_t* P;         // 2 planes x 8 x qb x r bf16
     int64_t q, r, qb, ranges, units, per;
 };
 
-template <int RUN>
+template <int RUNR, int RUNW>
 __global__ __launch_bounds__(512, 1) void tile_pattern(TileArgs a) {
-    constexpr int T = 512, PR = RUN / 16;   // lanes per row run
-    constexpr int LD = 24 * 16 * PR / T, ST = 16 * 16 * PR / T;
+    constexpr int RUN = RUNR > RUNW ? RUNR : RUNW;
+    constexpr int T = 512, PRr = RUNR / 16, PRw = RUNW / 16;   // lanes per row run
+    constexpr int LD = 24 * 16 * (RUN / 16) / T, ST = 16 * 16 * (RUN / 16) / T;
     const int tid = threadIdx.x;
     const int64_t u0 = static_cast<int64_t>(blockIdx.x) * a.per;
     const int64_t u1 = u0 + a.per < a.units ? u0 + a.per : a.units;
@@ -129,11 +131,13 @@ __global__ __launch_bounds__(512, 1) void tile_pattern(TileArgs a) {
         const int64_t t0 = (u / a.ranges) * 16, c0 = (u % a.ranges) * (RUN / 2);
 #pragma unroll
         for (int i = 0; i < LD; ++i) {
+            // piece e: run qq of the row outermost, then block row, then lane in the run
             const int e = tid + T * i;
-            const int j = e / (16 * PR), row = (e / PR) % 16, pc = e % PR;
+            const int pc = e % PRr, jrow = (e / PRr) % 384, qq = e / (PRr * 384);
+            const int j = jrow / 16, row = jrow % 16;
             const int64_t t = t0 + row < a.qb ? t0 + row : a.qb - 1;
             const int64_t g = j * a.qb + t < a.q ? j * a.qb + t : a.q - 1;
-            R[set][i] = *reinterpret_cast<const f4*>(a.A + g * a.r + c0 + pc * 8);
+            R[set][i] = *reinterpret_cast<const f4*>(a.A + g * a.r + c0 + (qq * PRr + pc) * 8);
         }
     };
     auto store = [&](int set, int64_t u) __attribute__((always_inline)) {
@@ -141,9 +145,10 @@ __global__ __launch_bounds__(512, 1) void tile_pattern(TileArgs a) {
 #pragma unroll
         for (int i = 0; i < ST; ++i) {
             const int e = tid + T * i;
-            const int pl = e / (16 * PR), row = (e / PR) % 16, pc = e % PR;
+            const int pc = e % PRw, prow = (e / PRw) % 256, qq = e / (PRw * 256);
+            const int pl = prow / 16, row = prow % 16;
             if (t0 + row < a.qb) {
-                const int64_t off = ((pl / 8) * 8 * a.qb + (pl % 8) * a.qb + t0 + row) * a.r + c0 + pc * 8;
+                const int64_t off = ((pl / 8) * 8 * a.qb + (pl % 8) * a.qb + t0 + row) * a.r + c0 + (qq * PRw + pc) * 8;
                 __builtin_nontemporal_store(R[set][i % LD] + R[set][(i + 1) % LD], reinterpret_cast<f4*>(a.P + off));
             }
         }
@@ -286,25 +291,25 @@ int calib_read_rows(const float* A, int64_t rows, int r, int pattern, int reps, 
 
 // The single pass's memory pattern (tile_pattern above) over a q x r bf16
 // matrix A (r a multiple of 256) and parity planes P of 2 x 8 x ceil(q/24) x r
-// bf16, both device buffers, with RUN = run bytes per row and unit (128, 256
-// or 512); one workgroup per compute unit (`cus`).  Bytes moved per launch:
-// 2 q r read + 4 x 8 x ceil(q/24) x r written.
-int calib_tile_pattern(const void* A, void* P, int64_t q, int64_t r, int run, int cus, int reps, float* ms) {
+// bf16, both device buffers, with read and write runs of run_read and
+// run_write bytes per row (128, 256 or 512 each; the pairs 128/128, 256/256,
+// 512/512 and 512/128); one workgroup per compute unit (`cus`).  Bytes moved
+// per launch: 2 q r read + 4 x 8 x ceil(q/24) x r written.
+int calib_tile_pattern(const void* A, void* P, int64_t q, int64_t r, int run_read, int run_write, int cus, int reps,
+                       float* ms) {
     if (q <= 0 || r <= 0 || r % 256 != 0 || cus <= 0) return 2;
     TileArgs a{static_cast<const uint16_t*>(A), static_cast<uint16_t*>(P), q, r, (q + 23) / 24, 0, 0, 0};
+    const int run = run_read > run_write ? run_read : run_write;
     a.ranges = r * 2 / run;
     a.units = (a.qb + 15) / 16 * a.ranges;
     a.per = (a.units + cus - 1) / cus;
     a.per = a.per > a.ranges ? a.per : a.ranges;
     const unsigned blocks = static_cast<unsigned>((a.units + a.per - 1) / a.per);
-    switch (run) {
-        case 128:
-            return time_ms([&] { hipLaunchKernelGGL(tile_pattern<128>, dim3(blocks), dim3(512), 0, nullptr, a); }, reps, ms);
-        case 256:
-            return time_ms([&] { hipLaunchKernelGGL(tile_pattern<256>, dim3(blocks), dim3(512), 0, nullptr, a); }, reps, ms);
-        case 512:
-            return time_ms([&] { hipLaunchKernelGGL(tile_pattern<512>, dim3(blocks), dim3(512), 0, nullptr, a); }, reps, ms);
-    }
+    auto go = [&](auto kernel) { return time_ms([&] { hipLaunchKernelGGL(kernel, dim3(blocks), dim3(512), 0, nullptr, a); }, reps, ms); };
+    if (run_read == 128 && run_write == 128) return go(tile_pattern<128, 128>);
+    if (run_read == 256 && run_write == 256) return go(tile_pattern<256, 256>);
+    if (run_read == 512 && run_write == 512) return go(tile_pattern<512, 512>);
+    if (run_read == 512 && run_write == 128) return go(tile_pattern<512, 128>);
     return 2;
 }
 
