@@ -15,9 +15,10 @@ from tests.gpu_helpers import device_tensor, make_inputs, normwise_rel_err, torc
 pytestmark = pytest.mark.gpu
 
 N, K = 32, 24
-# (q, r): ragged tile + padded block; shared tiles (300 tiles, 2 stages); no padding; one row in the last tile;
-# one row per block (one tile, one stage); a single row of A (every other block is padding)
-SHAPES = [(1000, 1024), (115200, 128), (1152, 192), (24 * 17, 64), (24, 64), (1, 128)]
+# (q, r): ragged tile + padded block; 300 tiles of 2 stages; 300 tiles of 5 stages (loaded in groups of four, so
+# each tile ends with three empty stages, and 12-unit runs split tiles between two workgroups); no padding; one
+# row in the last tile; one row per block (one tile, one stage); a single row of A (every other block is padding)
+SHAPES = [(1000, 1024), (115200, 128), (115200, 320), (1152, 192), (24 * 17, 64), (24, 64), (1, 128)]
 
 
 @pytest.fixture(scope="module")
@@ -81,7 +82,7 @@ def test_single_pass_gaussian(lib, torch, q, r):
     assert np.all(np.abs(Y - Y2) <= 4 * r * 2.0 ** -24 * mag)
 
 
-@pytest.mark.parametrize("q,r", [(1000, 1024), (115200, 128), (24 * 17, 64), (1, 64)])
+@pytest.mark.parametrize("q,r", [(1000, 1024), (115200, 128), (115200, 320), (24 * 17, 64), (1, 64)])
 def test_single_pass_integer_bit_exact(lib, torch, q, r):
     P, A, X = make_inputs(N, K, q, r, 64, 32, "bf16", integer=True)
     code, pe, pf, Y, Y2 = run_both(lib, torch, P, A, X)
