@@ -328,12 +328,21 @@ __device__ inline __amdgpu_buffer_rsrc_t y_buffer(const void* base, uint32_t byt
 // raw buffer, each lane's offset per survivor fixed for the set and the
 // group's offset in a scalar register, so the loads need no vector address
 // arithmetic.
+// Six waves per SIMD (80 registers, six workgroups per compute unit) for the
+// variants with whole survivor groups and buffer-addressed Y up to 12 groups,
+// which then spill one word in the elimination; the others keep the default
+// register budget.
+template <int KS, bool FULL, bool YBUF>
+constexpr int decode_min_waves() {
+    return FULL && YBUF && KS <= 12 ? 6 : 1;
+}
+
 template <int KS, int E, typename YT, bool FULL, bool YBUF>
-__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, DecodeSet single, int64_t chunks,
-                                                               int elems_per_block) {
+__global__ __launch_bounds__(kThreads, (decode_min_waves<KS, FULL, YBUF>())) void decode_mfma_kernel(
+    DecodeArgs a, DecodeSet single, int64_t chunks, int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
-    __shared__ double sOut[E == 4 ? kThreads / 64 : 1][E == 4 ? 256 * kDecodePE : 1];   // per-wave output tile
+    __shared__ double sOut[E == 4 ? kThreads / 64 - 1 : 1][E == 4 ? 256 * kDecodePE : 1];   // per combining wave output tile
     __shared__ int32_t sSimd[kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int k = a.k;
@@ -469,9 +478,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a, Dec
         // aligned, so the chunk bounds and the total are multiples of 4.)
         constexpr int PE = kDecodePE;
         constexpr int W = 16 * PE;
-        double* buf = sOut[wv];
         const int ngroups = (e1 - e0 + W - 1) / W;
         const int crank = __builtin_amdgcn_readfirstlane(wv < ew ? wv : wv - 1);   // rank among the combining waves
+        double* buf = sOut[crank];
         // each store instruction covers 16 / PE blocks, 4 PE lanes (W
         // elements, whole 128-byte lines for PE = 2) per block; this lane's
         // block, its first row in out and its element limit are fixed for the set
