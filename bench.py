@@ -517,13 +517,13 @@ def decode_workload(args):
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": algo_bytes,
                      "traffic": measured_kernel_traffic(w.name, "decode_mfma_kernel<12, 4, double, true, true>", algo_bytes), "fp64_tflops": flops / mean_s / 1e12, "fp64_frac": flops / mean_s / 78.6e12,
                      "mfma_counters": measured_mfma(w.name, "decode_mfma_kernel<12, 4, double, true, true>")},
-        "products": {"kernel": "gemm_f32_mfma_kernel<1, 2, true, 64, 4, true> (64 worker products, s = 8, once per run)",
+        "products": {"kernel": "gemm_f32_mfma_kernel<1, 2, true, 128, 2, true> (64 worker products, s = 8, once per run)",
                      "ms_mean": float(prod_ms.mean()), "ms_min": float(prod_ms.min()),
                      "algorithmic_bytes_per_launch": prod_bytes,
                      "achieved_gbs": prod_bytes / (float(prod_ms.mean()) * 1e-3) / 1e9,
                      "hbm_frac": prod_bytes / (float(prod_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBS,
                      "fp64_tflops": prod_flops / (float(prod_ms.mean()) * 1e-3) / 1e12,
-                     "traffic": measured_kernel_traffic(w.name, "gemm_f32_mfma_kernel<1, 2, true, 64, 4, true>", prod_bytes)},
+                     "traffic": measured_kernel_traffic(w.name, "gemm_f32_mfma_kernel<1, 2, true, 128, 2, true>", prod_bytes)},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)

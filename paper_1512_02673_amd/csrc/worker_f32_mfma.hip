@@ -386,7 +386,7 @@ bool gemm_f32_mfma_supported(const WorkerArgs& a) {
 // than one 64-column launch at s = 64: the wider tile halves occupancy).
 hipError_t launch_gemm_f32_mfma(const WorkerArgs& a, hipStream_t st) {
     if (a.s <= 4) return launch_mm<1, 1, true, 128, 4>(a, 0, st);
-    if (a.s <= 8) return launch_mm<1, 2, true, 64, 4>(a, 0, st);
+    if (a.s <= 8) return launch_mm<1, 2, true, 128, 2>(a, 0, st);
     for (int64_t c0 = 0; c0 < a.s; c0 += 32) {
         const hipError_t e = a.s - c0 <= 16 ? launch_mm<2, 1, false, 64, 2>(a, c0, st)
                                             : launch_mm<2, 2, false, 64, 2>(a, c0, st);
