@@ -145,8 +145,9 @@ coded_status coded_sizes(const coded_code* code, coded_dtype dt, coded_dtype y_d
  * q are the zero padding of Sec. III-A's footnote and are never read.
  *   dt        CODED_F32: sums in fp64; CODED_BF16: every P entry must be a
  *             bfloat16 value (else CODED_ERR_ARG), sums in fp32.  For bf16
- *             codes with k = 24, n - k = 8 and two planes, r a multiple of 64,
- *             lda a multiple of 8 and A, parity 16-byte aligned, each column's
+ *             codes with k = 24, n - k = 8 and two planes, r a multiple of 64
+ *             below 2^23, lda a multiple of 8 below 2^25 and A, parity
+ *             16-byte aligned, each column's
  *             sum is formed on the matrix cores (exact products, one fp32
  *             result); coded_encode_worker_mm writes the same planes.
  *   A         device, q x r of dt, row stride lda.
