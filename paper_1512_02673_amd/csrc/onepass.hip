@@ -27,6 +27,27 @@ typedef float f32x4o __attribute__((ext_vector_type(4)));
 
 __device__ inline f32x4o load4(const float* p) { return *reinterpret_cast<const f32x4o*>(p); }
 
+// Sum of v over the wavefront, in every lane: cross-lane moves within each
+// 16-lane row (DPP: quad swaps, then half-row and row mirrors), then the
+// four row sums read from lanes 0, 16, 32 and 48.  No LDS round trips.
+template <int CTRL>
+__device__ inline double dpp_f64(double v) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const uint32_t lo = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, 0xF, 0xF, false));
+    const uint32_t hi = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, 0xF, 0xF, false));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+__device__ inline double wave_total(double v) {
+    v += dpp_f64<0xB1>(v);    // quad_perm [1,0,3,2]
+    v += dpp_f64<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dpp_f64<0x141>(v);   // row_half_mirror
+    v += dpp_f64<0x140>(v);   // row_mirror: every lane holds its row's sum
+    return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
+}
+
 __device__ inline double dot4(f32x4o a, f32x4o x, double acc) {
     acc = fma(static_cast<double>(a.x), static_cast<double>(x.x), acc);
     acc = fma(static_cast<double>(a.y), static_cast<double>(x.y), acc);
@@ -144,7 +165,7 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
 #pragma unroll
     for (int i = 0; i < MN; ++i) {
         if (i < n) {
-            const double v = wave_sum(y[i]);
+            const double v = wave_total(y[i]);
             if (lane == 0) red[wv][i] = v;
         }
     }
