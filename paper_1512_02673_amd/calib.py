@@ -82,7 +82,7 @@ def ceilings(read_bytes: int = 3 * 2 ** 30, reps: int = 20) -> dict:
         f"reads {1024 // rr} rows x {rr} B, writes {1024 // rw} rows x {rw} B per wave instruction":
             moved / (_ms(h.calib_tile_pattern, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(P.data_ptr()), q, r, rr,
                          rw, cus, 5) * 1e-3) / 1e9
-        for rr, rw in ((128, 128), (256, 256), (512, 512), (512, 128))}
+        for rr, rw in ((128, 128), (256, 256), (512, 512), (512, 128), (512, 256))}
     del A, P
     rates = {}
     kinds = [("v_mfma_f64_16x16x4f64", 0, 2000), ("v_mfma_f64_4x4x4f64", 1, 4000),

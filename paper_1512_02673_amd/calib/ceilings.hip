@@ -293,7 +293,7 @@ int calib_read_rows(const float* A, int64_t rows, int r, int pattern, int reps, 
 // matrix A (r a multiple of 256) and parity planes P of 2 x 8 x ceil(q/24) x r
 // bf16, both device buffers, with read and write runs of run_read and
 // run_write bytes per row (128, 256 or 512 each; the pairs 128/128, 256/256,
-// 512/512 and 512/128); one workgroup per compute unit (`cus`).  Bytes moved
+// 512/512, 512/128 and 512/256); one workgroup per compute unit (`cus`).  Bytes moved
 // per launch: 2 q r read + 4 x 8 x ceil(q/24) x r written.
 int calib_tile_pattern(const void* A, void* P, int64_t q, int64_t r, int run_read, int run_write, int cus, int reps,
                        float* ms) {
@@ -310,6 +310,7 @@ int calib_tile_pattern(const void* A, void* P, int64_t q, int64_t r, int run_rea
     if (run_read == 256 && run_write == 256) return go(tile_pattern<256, 256>);
     if (run_read == 512 && run_write == 512) return go(tile_pattern<512, 512>);
     if (run_read == 512 && run_write == 128) return go(tile_pattern<512, 128>);
+    if (run_read == 512 && run_write == 256) return go(tile_pattern<512, 256>);
     return 2;
 }
 
