@@ -567,6 +567,7 @@ coded_status coded_matmul(const coded_code* c, coded_dtype dt, const void* A, in
         oa.k = c->k;
         oa.planes = c->planes;
         oa.encode = parity_ready ? 0 : 1;
+        oa.missing = m;
         const hipError_t e = launch_onepass_f32(oa, st);
         if (e != hipSuccess) return hip_fail(e, "one-pass product launch");
         if (survivors_out) std::copy(surv, surv + c->k, survivors_out);

@@ -19,6 +19,7 @@ struct OnePassArgs {
     DecodeSet set;        // the k survivors, checked on the host
     int64_t q, r, lda, qb, ldo;
     int32_t n, k, planes, encode;
+    int32_t missing;      // survivors at or past k (the blocks to solve for), from the same set
 };
 bool onepass_supported(int n, int k, int64_t q, int64_t r, int64_t lda, const void* A, const void* parity,
                        const void* x);

@@ -27,6 +27,12 @@ typedef float f32x4o __attribute__((ext_vector_type(4)));
 
 __device__ inline f32x4o load4(const float* p) { return *reinterpret_cast<const f32x4o*>(p); }
 
+// Pointers into device (global) memory, so that loads through them stay
+// global loads once the compiler can no longer trace them to an argument.
+typedef __attribute__((address_space(1))) const float gfloat;
+typedef __attribute__((address_space(1))) const f32x4o gf32x4o;
+__device__ inline f32x4o load4(const gfloat* p) { return *reinterpret_cast<const gf32x4o*>(p); }
+
 // Sum of v over the wavefront, in every lane: cross-lane moves within each
 // 16-lane row (DPP: quad swaps, then half-row and row mirrors), then the
 // four row sums read from lanes 0, 16, 32 and 48.  No LDS round trips.
@@ -48,6 +54,39 @@ __device__ inline double wave_total(double v) {
     return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
 }
 
+// The set's bookkeeping, by one wave (the host has validated the set; k <= n
+// <= 16, so lane j stands for block j).  The survivors form a bit mask; from
+// it every entry is written by one lane without reading another's: the
+// survivors in ascending order, presence, the missing systematic blocks in
+// ascending order, and the rows of each block that lie inside A.  No
+// workgroup barrier: the wave orders its own LDS writes before its
+// elimination reads them, and the other waves read them after the barrier
+// that precedes the decode.  Returns the number of missing blocks.
+__device__ inline int setup_set_wave(const OnePassArgs& a, int lane, SetMeta& sm) {
+    const int n = a.n, k = a.k;
+    uint32_t mask = 0;
+    for (int c = 0; c < k; ++c) mask |= 1u << set_entry(a.set, c);
+    const uint32_t below = static_cast<uint32_t>((uint64_t{1} << lane) - 1u);   // blocks below this lane's
+    const bool in = lane < 32 && ((mask >> lane) & 1u) != 0;
+    if (lane < n) {
+        sm.present[lane] = in ? 1 : 0;
+        if (in) sm.S[__builtin_popcount(mask & below)] = lane;
+    }
+    if (lane < k) {
+        if (!in) sm.miss[__builtin_popcount(~mask & below)] = lane;
+        const int64_t lim = a.q - static_cast<int64_t>(lane) * a.qb;
+        sm.lim[lane] = static_cast<int32_t>(lim < 0 ? 0 : (lim > a.qb ? a.qb : lim));
+    }
+    const int m = k - __builtin_popcount(mask & ((1u << k) - 1u));
+    if (lane == 0) {
+        sm.status = 0;
+        sm.m = m;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    return m;
+}
+
 __device__ inline double dot4(f32x4o a, f32x4o x, double acc) {
     acc = fma(static_cast<double>(a.x), static_cast<double>(x.x), acc);
     acc = fma(static_cast<double>(a.y), static_cast<double>(x.y), acc);
@@ -66,56 +105,69 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
     __shared__ double red[NW][MN];
     __shared__ double sy[MN];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int n = a.n, k = a.k, npar = n - k;
     const int64_t t = blockIdx.x;
+    // The arguments the first loads depend on, fetched in one batch before
+    // anything else and then held in scalar registers (left alone, the
+    // compiler fetches each inside the branch that first uses it, one
+    // dependent round trip after another before the first load goes out).
+    const gfloat* Ap = (const gfloat*)a.A;
+    const gfloat* xp = (const gfloat*)a.x;
+    int64_t q = a.q, qb = a.qb, r = a.r, lda = a.lda;
+    int32_t n = a.n, k = a.k, missing = a.missing;
+    asm volatile("" : "+s"(Ap), "+s"(xp), "+s"(q), "+s"(qb), "+s"(r), "+s"(lda), "+s"(n), "+s"(k), "+s"(missing));
+    const int npar = n - k;
     int kin = 0;                                  // data blocks whose row t lies inside A
-    while (kin < k && static_cast<int64_t>(kin) * a.qb + t < a.q) ++kin;
-    int m0 = 0;                                   // missing blocks: survivors at or past k
-    for (int c = 0; c < k; ++c) m0 += set_entry(a.set, c) >= k ? 1 : 0;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) kin += (j < k && static_cast<int64_t>(j) * qb + t < q) ? 1 : 0;
     // With blocks to solve for, wave 0 forms D while the other waves stream
     // the columns (the two chains run side by side); otherwise all stream.
-    const int cw = (m0 > 0 && NW > 1) ? 1 : 0;
+    const int cw = (missing > 0 && NW > 1) ? 1 : 0;
 
     // This thread's first columns are requested before anything else, so the
     // memory latency overlaps the set bookkeeping and the elimination.
     auto load_chunk = [&](int64_t c, f32x4o (&av)[KM], f32x4o& xv) __attribute__((always_inline)) {
-        xv = load4(a.x + c);
+        xv = load4(xp + c);
 #pragma unroll
         for (int j = 0; j < KM; ++j) {
             av[j] = f32x4o{0.f, 0.f, 0.f, 0.f};
-            if (j < kin) av[j] = load4(a.A + (static_cast<int64_t>(j) * a.qb + t) * a.lda + c);
+            if (j < kin) av[j] = load4(Ap + (static_cast<int64_t>(j) * qb + t) * lda + c);
         }
     };
     f32x4o avA[KM], avB[KM], xA, xB;
     const int64_t kStep = static_cast<int64_t>(NT - 64 * cw) * 4;
-    int64_t c = wv < cw ? a.r : static_cast<int64_t>(tid - 64 * cw) * 4;
-    if (c < a.r) load_chunk(c, avA, xA);
+    int64_t c = wv < cw ? r : static_cast<int64_t>(tid - 64 * cw) * 4;
+    if (c < r) load_chunk(c, avA, xA);
 
-    DecodeArgs da{};
-    da.G = a.G;
-    da.info = a.info;
-    da.q = a.q;
-    da.qb = a.qb;
-    da.s = 1;
-    da.ldo = a.ldo;
-    da.n = n;
-    da.k = k;
-    da.batch = 1;
-    setup_set<NT>(da, a.set, 0, false, sm);     // the host has checked the set
-    const int m = sm.m;
-    if (m > 0 && wv == 0) eliminate_set(da, sm, m, k - m, lane, sD);   // read after the barrier below
+    // Wave 0 sets up the set and forms D (read by all after the barrier
+    // below); the streaming waves go straight on to their columns.
+    if (wv == 0) {
+        const int m = setup_set_wave(a, lane, sm);
+        if (m > 0) {
+            DecodeArgs da{};
+            da.G = a.G;
+            da.info = a.info;
+            da.q = q;
+            da.qb = qb;
+            da.s = 1;
+            da.ldo = a.ldo;
+            da.n = n;
+            da.k = k;
+            da.batch = 1;
+            eliminate_set(da, sm, m, k - m, lane, sD);
+        }
+    }
 
     // Row t of the data blocks (zero past q), the parity rows, and the n products.
     double y[MN];
 #pragma unroll
     for (int i = 0; i < MN; ++i) y[i] = 0.0;
-    const int64_t plane = static_cast<int64_t>(npar) * a.qb * a.r;
+    const int64_t plane = static_cast<int64_t>(npar) * qb * r;
     auto process = [&](int64_t c, const f32x4o (&av)[KM], f32x4o xv) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < KM; ++j)
             if (j < kin) y[j] = dot4(av[j], xv, y[j]);
         for (int p = 0; p < npar; ++p) {
-            float* prow = a.parity + (static_cast<int64_t>(p) * a.qb + t) * a.r + c;
+            float* prow = a.parity + (static_cast<int64_t>(p) * qb + t) * r + c;
             const double* g = a.G + static_cast<int64_t>(k + p) * k;    // parity row p of G (uniform)
             f32x4o hi, lo = f32x4o{0.f, 0.f, 0.f, 0.f};
             if (a.encode) {
@@ -153,12 +205,12 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
         }
     };
     // one chunk of loads in flight ahead of the chunk being combined
-    while (c < a.r) {
-        if (c + kStep < a.r) load_chunk(c + kStep, avB, xB);
+    while (c < r) {
+        if (c + kStep < r) load_chunk(c + kStep, avB, xB);
         process(c, avA, xA);
         c += kStep;
-        if (c >= a.r) break;
-        if (c + kStep < a.r) load_chunk(c + kStep, avA, xA);
+        if (c >= r) break;
+        if (c + kStep < r) load_chunk(c + kStep, avA, xA);
         process(c, avB, xB);
         c += kStep;
     }
