@@ -135,3 +135,36 @@ def test_one_pass_singular_set_leaves_out_untouched(lib, torch):
     G = oc.systematic_generator(P)
     ref = oc.worker_products(oc.encode(G, oc.pad_and_split(A, k)), x[:, None])[..., 0]
     assert np.array_equal(Y, ref)
+
+
+@pytest.mark.parametrize("n,k,q,r", [(4, 2, 2048, 512), (6, 4, 1001, 260), (16, 8, 2000, 2048)])
+def test_one_pass_every_missing_count(lib, torch, n, k, q, r):
+    """Draws chosen so that every number of missing systematic blocks occurs,
+    from none (wave 0 streams beside the others and forms no decoding
+    matrix) to min(k, n - k) (the most parity survivors a set can hold): the
+    set bookkeeping wave 0 builds from the survivors' bit mask must give the
+    separate steps' outputs in each case."""
+    seed = 43
+    P, A, X = make_inputs(n, k, q, r, 1, seed)
+    code = lib.Code.systematic(P, 2)
+    dA, dx = device_tensor(A), device_tensor(X[:, 0])
+    par = lib.alloc_parity(code, q, r, torch.float32)
+    ref = oc.plain_product(A, X)
+    wanted = set(range(min(k, n - k) + 1))
+    draws = {}
+    for d in range(20000):
+        m = int(np.sum(oc.draw_survivors(n, k, seed, d)[0] >= k))
+        draws.setdefault(m, d)
+        if wanted <= set(draws):
+            break
+    assert wanted <= set(draws), f"no draw with m in {sorted(wanted - set(draws))}"
+    for m in sorted(wanted):
+        out, surv, Y1, info = one_pass(lib, torch, code, dA, par, dx, q, seed, draws[m], parity_ready=False)
+        assert info == 0 and int(np.sum(surv >= k)) == m
+        p3, Y3, out3, info3 = three_steps(lib, torch, code, dA, dx, q, r, surv)
+        assert info3 == 0 and torch.equal(par, p3)
+        planes_np = np.abs(p3.cpu().numpy().astype(np.float64)).sum(axis=0)
+        mag = oc.worker_products(np.concatenate([np.abs(oc.pad_and_split(A, k)), planes_np]), np.abs(X))[..., 0]
+        assert np.all(np.abs(Y1 - Y3) <= 2 * r * 2.0 ** -52 * mag)
+        assert normwise_rel_err(out, out3) <= 1e-6
+        assert normwise_rel_err(out, ref) <= 1e-4
