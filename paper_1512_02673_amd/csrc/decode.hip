@@ -339,15 +339,26 @@ constexpr int decode_min_waves() {
 
 template <int KS, int E, typename YT, bool FULL, bool YBUF>
 __global__ __launch_bounds__(kThreads, (decode_min_waves<KS, FULL, YBUF>())) void decode_mfma_kernel(
-    DecodeArgs a, DecodeSet single, int64_t chunks, int elems_per_block) {
+    DecodeArgs args, DecodeSet single, int64_t chunks, int elems_per_block) {
     __shared__ SetMeta sm;
     __shared__ double sD[64 * kFastLd];
     __shared__ double sOut[E == 4 ? kThreads / 64 - 1 : 1][E == 4 ? 256 * kDecodePE : 1];   // per combining wave output tile
     __shared__ int32_t sSimd[kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    DecodeArgs a = args;
+    if constexpr (E == 1) {
+        // Short chunks, latency bound: the sizes the set-up and the first
+        // loads depend on are fetched in one batch and held in scalar
+        // registers (left alone, the compiler fetches them one dependent
+        // round trip after another).
+        asm volatile("" : "+s"(a.q), "+s"(a.qb), "+s"(a.s), "+s"(a.ldo), "+s"(a.n), "+s"(a.k), "+s"(chunks),
+                     "+s"(elems_per_block));
+    }
     const int k = a.k;
-    const int64_t b = blockIdx.x / chunks;
-    const int64_t chunk = blockIdx.x % chunks;
+    // fewer than 2^31 workgroups (checked at launch): 32-bit division
+    const uint32_t bid = blockIdx.x, nch = static_cast<uint32_t>(chunks);
+    const int64_t b = bid / nch;
+    const int64_t chunk = bid - static_cast<uint32_t>(b) * nch;
     const bool writer = (chunk == 0 && tid == 0);
     if (lane == 0) sSimd[wv] = simd_id();             // read after setup_set's barriers
     if (!setup_set<kThreads>(a, single, b, writer, sm)) return;
@@ -385,6 +396,23 @@ __global__ __launch_bounds__(kThreads, (decode_min_waves<KS, FULL, YBUF>())) voi
                     cy[i] = Y[sm.yoff[c] + e];
                     co[i] = sm.ooff[w] + static_cast<int64_t>(t) * a.ldo + col;
                 }
+            }
+        }
+    }
+
+    // E == 1: each wave's first tile of Y (Y_{S[4 st + lk]} at element li of
+    // the tile, as the tile loop below reads it) is requested before the
+    // barrier that publishes D, so its latency overlaps the elimination.
+    const int ntiles1 = (e1 - e0 + 15) / 16;
+    YT yfirst[E == 1 ? KS : 1];
+    if constexpr (E == 1) {
+        if (m > 0 && wv < ntiles1) {
+            const int li = lane & 15, lk = lane >> 4;
+            const int el = min(e0 + wv * 16 + li, e1 - 1);
+#pragma unroll
+            for (int st = 0; st < KS; ++st) {
+                const int c = 4 * st + lk;
+                yfirst[st] = Y[(c < k ? static_cast<int32_t>(sm.yoff[c]) : 0) + el];
             }
         }
     }
@@ -566,16 +594,16 @@ __global__ __launch_bounds__(kThreads, (decode_min_waves<KS, FULL, YBUF>())) voi
             }
         }
     } else {
-        const int ntiles = (e1 - e0 + 15) / 16;
-        for (int tile = wv; tile < ntiles; tile += kWaves) {
+        for (int tile = wv; tile < ntiles1; tile += kWaves) {
             const int e = e0 + tile * 16 + li;
-            // Straight-line loads, all issued before the first is used.  A lane
-            // past the chunk's end reads its last element instead: column li of
-            // the product depends on column li of Y only, and is not stored.
+            // Straight-line loads, all issued before the first is used (the
+            // first tile's before the barrier).  A lane past the chunk's end
+            // reads its last element instead: column li of the product
+            // depends on column li of Y only, and is not stored.
             const int el = min(e, e1 - 1);
             YT yv[KS];
 #pragma unroll
-            for (int st = 0; st < KS; ++st) yv[st] = Y[yo[st] + el];
+            for (int st = 0; st < KS; ++st) yv[st] = tile == wv ? yfirst[st] : Y[yo[st] + el];
             f64x4v acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int st = 0; st < KS; ++st) {
