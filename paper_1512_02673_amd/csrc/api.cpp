@@ -78,8 +78,6 @@ size_t dtype_size(coded_dtype d) {
     return 0;
 }
 
-bool valid_dtype(coded_dtype d) { return d == CODED_F32 || d == CODED_BF16 || d == CODED_F64; }
-
 coded_status check_dt(coded_dtype dt, coded_dtype y_dt) {
     if (dt != CODED_F32 && dt != CODED_BF16) return fail(CODED_ERR_ARG, "dt must be CODED_F32 or CODED_BF16");
     if (dt == CODED_F32 && y_dt != CODED_F64 && y_dt != CODED_F32)
@@ -360,9 +358,10 @@ coded_status coded_code_create(int32_t n, int32_t k, const double* G, int32_t pl
 coded_status coded_code_destroy(coded_code* c) {
     CODED_GUARD_BEGIN
     if (!c) return CODED_OK;
-    for (hipEvent_t ev : c->worker_events) hipEventDestroy(ev);
-    if (c->start_event) hipEventDestroy(c->start_event);
-    for (hipStream_t w : c->worker_streams) hipStreamDestroy(w);
+    // teardown: a failure to release one handle must not stop the others
+    for (hipEvent_t ev : c->worker_events) (void)hipEventDestroy(ev);
+    if (c->start_event) (void)hipEventDestroy(c->start_event);
+    for (hipStream_t w : c->worker_streams) (void)hipStreamDestroy(w);
     delete c;
     return CODED_OK;
     CODED_GUARD_END
@@ -631,9 +630,10 @@ coded_status ensure_straggler_state(coded_code* c) {
         if (e == hipSuccess) events.push_back(ev);
     }
     if (e != hipSuccess) {
-        for (hipEvent_t ev : events) hipEventDestroy(ev);
-        for (hipStream_t w : streams) hipStreamDestroy(w);
-        if (start) hipEventDestroy(start);
+        // undo what was created; the first error is the one reported
+        for (hipEvent_t ev : events) (void)hipEventDestroy(ev);
+        for (hipStream_t w : streams) (void)hipStreamDestroy(w);
+        if (start) (void)hipEventDestroy(start);
         return hip_fail(e, "straggler streams and events");
     }
     c->worker_streams = std::move(streams);
