@@ -87,6 +87,35 @@ __device__ inline int setup_set_wave(const OnePassArgs& a, int lane, SetMeta& sm
     return m;
 }
 
+__device__ inline double lane_xor(double v, int lane, int mask) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const int addr = (lane ^ mask) * 4;
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(addr, static_cast<int>(static_cast<uint32_t>(u))));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(addr, static_cast<int>(static_cast<uint32_t>(u >> 32))));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// Sums of four values v0..v3 over the wavefront at once: the first two
+// exchanges (lanes 1 and 2 apart) halve the values a lane carries, so that
+// lane l keeps value ((l & 1) << 1) | ((l >> 1) & 1) summed over its quad;
+// rotations by 4 and 8 within each 16-lane row and exchanges 16 and 32 lanes
+// apart then add the quads of the wavefront.  Lane l < 4 returns the total
+// of that value.
+__device__ inline double quad_class_total(double v0, double v1, double v2, double v3, int lane) {
+    const bool b0 = (lane & 1) != 0, b1 = (lane & 2) != 0;
+    // lanes 1 apart: keep values 2 b0 and 2 b0 + 1, send the other pair
+    const double k0 = b0 ? v2 : v0, k1 = b0 ? v3 : v1;
+    const double s0 = b0 ? v0 : v2, s1 = b0 ? v1 : v3;
+    const double z0 = k0 + dpp_f64<0xB1>(s0), z1 = k1 + dpp_f64<0xB1>(s1);
+    // lanes 2 apart: keep value 2 b0 + b1
+    double w = (b1 ? z1 : z0) + dpp_f64<0x4E>(b1 ? z0 : z1);
+    w += dpp_f64<0x124>(w);   // row_ror:4
+    w += dpp_f64<0x128>(w);   // row_ror:8: every lane holds its row's sum of its value
+    w += lane_xor(w, lane, 16);
+    w += lane_xor(w, lane, 32);
+    return w;
+}
+
 __device__ inline double dot4(f32x4o a, f32x4o x, double acc) {
     acc = fma(static_cast<double>(a.x), static_cast<double>(x.x), acc);
     acc = fma(static_cast<double>(a.y), static_cast<double>(x.y), acc);
@@ -214,11 +243,18 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
         process(c, avB, xB);
         c += kStep;
     }
+    if (n <= 4) {
+        // lane l < 4 holds the total of value ((l & 1) << 1) | ((l >> 1) & 1)
+        const double v = quad_class_total(y[0], y[1], y[2], y[3], lane);
+        const int i = ((lane & 1) << 1) | ((lane >> 1) & 1);
+        if (lane < 4 && i < n) red[wv][i] = v;
+    } else {
 #pragma unroll
-    for (int i = 0; i < MN; ++i) {
-        if (i < n) {
-            const double v = wave_total(y[i]);
-            if (lane == 0) red[wv][i] = v;
+        for (int i = 0; i < MN; ++i) {
+            if (i < n) {
+                const double v = wave_total(y[i]);
+                if (lane == 0) red[wv][i] = v;
+            }
         }
     }
     __syncthreads();
