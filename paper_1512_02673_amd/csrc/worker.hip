@@ -24,7 +24,14 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // 16-byte streaming load: the data is used once, so it is marked non-temporal
 // to keep it from displacing X in the caches.
 __device__ inline float4 load_stream(const float* p) {
-    const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    // a global-memory pointer, so the load is a global (not flat) load
+    typedef const __attribute__((address_space(1))) f32x4* gptr;
+    const f32x4 v = __builtin_nontemporal_load((gptr)(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ inline float4 load_global4(const float* p) {
+    typedef const __attribute__((address_space(1))) f32x4* gptr;
+    const f32x4 v = *(gptr)(p);
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
@@ -95,28 +102,43 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
     constexpr int kChunk = NT * 4 * XR;
     __shared__ double red[NW][T];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int64_t groups = ceil_div(a.qb, T);
-    const int64_t npar = groups * a.n_par;
-    const int64_t g = blockIdx.x;
+    // The arguments the first loads depend on, fetched in one batch and held
+    // in scalar registers (left alone, the compiler fetches them one
+    // dependent round trip after another, inside the branches that use them).
+    const float* Ap = static_cast<const float*>(a.A);
+    const float* Pp = static_cast<const float*>(a.parity);
+    const float* x = static_cast<const float*>(a.X);
+    int64_t q = a.q, r = a.r, lda = a.lda, qb = a.qb;
+    int32_t n = a.n, k = a.k, planes = a.planes, n_sys = a.n_sys, n_par = a.n_par;
+    asm volatile("" : "+s"(Ap), "+s"(Pp), "+s"(x), "+s"(q), "+s"(r), "+s"(lda), "+s"(qb), "+s"(n), "+s"(k),
+                 "+s"(planes), "+s"(n_sys), "+s"(n_par));
+    // The grid has fewer than 2^31 workgroups (checked at launch), so the
+    // tile arithmetic fits 32 bits.
+    const uint32_t groups = static_cast<uint32_t>(ceil_div(qb, T));
+    const uint32_t npar = groups * static_cast<uint32_t>(n_par);
+    const uint32_t g = blockIdx.x;
     int worker;
     int64_t grp;
     bool parity;
     // Parity workgroups stream `planes` times the bytes: dispatch them first so
-    // the launch does not end on a tail of long workgroups.
+    // the launch does not end on a tail of long workgroups.  With every worker
+    // active (the usual case) the worker follows from the index; otherwise
+    // from the lists of active workers.
     if (g < npar) {
-        worker = a.par_ids[g / groups];
-        grp = g % groups;
+        const uint32_t wi = g / groups;
+        worker = n_par == n - k ? k + static_cast<int>(wi) : a.par_ids[wi];
+        grp = g - wi * groups;
         parity = true;
     } else {
-        if (g - npar >= groups * a.n_sys) return;
-        worker = a.sys_ids[(g - npar) / groups];
-        grp = (g - npar) % groups;
+        if (g - npar >= groups * static_cast<uint32_t>(n_sys)) return;
+        const uint32_t wi = (g - npar) / groups;
+        worker = n_sys == k ? static_cast<int>(wi) : a.sys_ids[wi];
+        grp = (g - npar) - wi * groups;
         parity = false;
     }
     const int64_t t0 = grp * T;
-    const int nplanes = parity ? a.planes : 1;
-    const int64_t plane = static_cast<int64_t>(a.n - a.k) * a.qb * a.r;
-    const float* x = static_cast<const float*>(a.X);
+    const int nplanes = parity ? planes : 1;
+    const int64_t plane = static_cast<int64_t>(n - k) * qb * r;
 
     // Row pointers of the tile (null: padding row or beyond the block).
     const float* rows[T][2];
@@ -126,17 +148,17 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
         const int64_t t = t0 + i;
         rows[i][0] = rows[i][1] = nullptr;
         lo16[i] = nullptr;
-        if (t >= a.qb) continue;
+        if (t >= qb) continue;
         if (!parity) {
-            const int64_t rr = static_cast<int64_t>(worker) * a.qb + t;
-            if (rr < a.q) rows[i][0] = static_cast<const float*>(a.A) + rr * a.lda;
+            const int64_t rr = static_cast<int64_t>(worker) * qb + t;
+            if (rr < q) rows[i][0] = Ap + rr * lda;
         } else {
-            const int64_t off = (static_cast<int64_t>(worker - a.k) * a.qb + t) * a.r;
-            const float* base = static_cast<const float*>(a.parity) + off;
+            const int64_t off = (static_cast<int64_t>(worker - k) * qb + t) * r;
+            const float* base = Pp + off;
             rows[i][0] = base;
             if (nplanes == 2) {
                 if constexpr (LO16)
-                    lo16[i] = lo16_base(a) + off;
+                    lo16[i] = reinterpret_cast<const uint16_t*>(Pp + plane) + off;
                 else
                     rows[i][1] = base + plane;
             }
@@ -147,12 +169,12 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
 #pragma unroll
     for (int i = 0; i < T; ++i) acc[i] = 0.0;
 
-    for (int64_t cb = 0; cb < a.r; cb += kChunk) {
+    for (int64_t cb = 0; cb < r; cb += kChunk) {
         float4 xv[XR];
 #pragma unroll
         for (int j = 0; j < XR; ++j) {
             const int64_t c = cb + tid * 4 + j * NT * 4;
-            xv[j] = c < a.r ? *reinterpret_cast<const float4*>(x + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+            xv[j] = c < r ? load_global4(x + c) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
         for (int i = 0; i < T; ++i) {
@@ -169,7 +191,7 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
                     if constexpr (LO16) {
                         if (h == 1) continue;
                     }
-                    av[j] = c < a.r ? load_stream(row + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+                    av[j] = c < r ? load_stream(row + c) : make_float4(0.f, 0.f, 0.f, 0.f);
                 }
                 if constexpr (LO16) {
                     if (h == 1) {
@@ -177,7 +199,7 @@ __global__ __launch_bounds__(NT) void gemv_wg_kernel(WorkerArgs a) {
 #pragma unroll
                         for (int j = 0; j < XR; ++j) {
                             const int64_t c = cb + tid * 4 + j * NT * 4;
-                            raw[j] = c < a.r ? load_stream_bf16x4(lo16[i] + c) : u32x2{0u, 0u};
+                            raw[j] = c < r ? load_stream_bf16x4(lo16[i] + c) : u32x2{0u, 0u};
                         }
 #pragma unroll
                         for (int j = 0; j < XR; ++j) av[j] = widen_bf16x4(raw[j]);
@@ -265,11 +287,15 @@ hipError_t launch_gemv_wg(const WorkerArgs& a, hipStream_t st) {
     const int64_t blocks = ceil_div(a.qb, T) * (a.n_sys + a.n_par);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    // Rows of 8 column slots per thread: at most three workgroups per compute
+    // unit (each requests 40 KB of the 160 KB of LDS, which it does not use),
+    // which streams these long rows best (measured: two, three and four).
+    const size_t cap = XR >= 8 ? 40 * 1024 : 0;
     if (a.lo_bf16 && a.planes == 2)
-        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, true>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
-                           a);
+        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, true>), dim3(static_cast<unsigned>(blocks)), dim3(256), cap,
+                           st, a);
     else
-        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, false>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+        hipLaunchKernelGGL((gemv_wg_kernel<T, XR, 256, false>), dim3(static_cast<unsigned>(blocks)), dim3(256), cap,
                            st, a);
     return hipGetLastError();
 }
