@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "internal.h"
+#include "fused.h"
 #include "onepass.h"
 
 namespace coded {
@@ -210,15 +211,8 @@ coded_status do_encode_workers(const coded_code* c, coded_dtype dt, const void* 
     for (size_t i = static_cast<size_t>(c->k) * c->k; i < c->G.size(); ++i)
         if (!is_bf16_value(c->G[i]))
             return fail(CODED_ERR_ARG, "bf16 encode needs every parity coefficient to be a bfloat16 value");
-    WorkerArgs xa{};
-    xa.X = X;
-    xa.r = r;
-    xa.s = s;
-    xa.ldx = ldx;
-    xa.xt = workspace;
-    hipError_t e = launch_transpose_x_bf16(xa, st);
-    if (e == hipSuccess)
-        e = launch_fused_bf16(fused_args(c, A, q, r, lda, parity, workspace, Y), true, c->compute_units, st);
+    const hipError_t e = launch_fused_bf16_from_x(fused_args(c, A, q, r, lda, parity, workspace, Y),
+                                                  static_cast<const uint16_t*>(X), s, ldx, c->compute_units, st);
     if (e != hipSuccess) return hip_fail(e, "encode and worker launch");
     return CODED_OK;
 }

@@ -42,6 +42,7 @@
 // the same piece in 8 or 16 consecutive rows, and a row write, touch distinct
 // banks.
 #include "internal.h"
+#include "fused.h"
 
 namespace coded {
 namespace {
@@ -373,28 +374,46 @@ __global__ void zero_f32_kernel(float* p, int64_t n) {
         for (int64_t j = i; j < n; ++j) p[j] = 0.0f;
 }
 
+// What the single pass with products needs before it starts, in one launch:
+// X (r x s bf16, row stride ldx) transposed into XT (s x r) by the first
+// `ttiles` workgroups, 64 x 64 tiles through LDS, and Y (ny floats) zeroed by
+// the others, 4096 floats each with 16-byte stores.
+__global__ __launch_bounds__(256) void fused_prep_kernel(const uint16_t* __restrict__ X, int64_t r, int64_t s,
+                                                         int64_t ldx, uint16_t* __restrict__ XT, int64_t tiles_s,
+                                                         int64_t ttiles, float* __restrict__ Y, int64_t ny) {
+    __shared__ uint16_t tile[64][65];
+    const int64_t bid = blockIdx.x;
+    if (bid < ttiles) {
+        const int64_t tr = bid / tiles_s, ts = bid % tiles_s;
+        const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+        for (int i = ty; i < 64; i += 4) {
+            const int64_t k = tr * 64 + i, c = ts * 64 + tx;
+            tile[i][tx] = (k < r && c < s) ? X[k * ldx + c] : static_cast<uint16_t>(0);
+        }
+        __syncthreads();
+        for (int i = ty; i < 64; i += 4) {
+            const int64_t c = ts * 64 + i, k = tr * 64 + tx;
+            if (c < s && k < r) XT[c * r + k] = tile[tx][i];
+        }
+        return;
+    }
+    const int64_t base = (bid - ttiles) * 4096 + threadIdx.x * 4;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t i = base + u * 1024;
+        if (i + 4 <= ny)
+            *reinterpret_cast<f32x4f*>(Y + i) = f32x4f{0.f, 0.f, 0.f, 0.f};
+        else
+            for (int64_t j = i; j < ny; ++j) Y[j] = 0.0f;
+    }
+}
+
 // Eight wavefronts per workgroup (two per SIMD): each owns three systematic
 // blocks and one parity row of the products and one 8-column group of the
 // encode.
 constexpr int kWaves = 8;
 
-}  // namespace
-
-bool fused_bf16_supported(int n, int k, int planes, int64_t r, int64_t lda) {
-    // a 64-row buffer of X^T and a 16-row tile of A must stay below 2^31 bytes
-    return planes == 2 && k == 24 && n - k == 8 && r > 0 && r % kStage == 0 && lda % 8 == 0 && r < (1 << 23) &&
-           lda < (1 << 25);
-}
-
-hipError_t launch_fused_bf16(FusedArgs a, bool products, int compute_units, hipStream_t st) {
-    if (a.qb == 0 || a.r == 0) return hipSuccess;
-    hipError_t e;
-    if (products) {
-        const int64_t ny = static_cast<int64_t>(a.n) * a.qb * 64;
-        hipLaunchKernelGGL(zero_f32_kernel, dim3(static_cast<unsigned>(ceil_div(ny, 4 * 256))), dim3(256), 0, st, a.Y,
-                           ny);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+hipError_t launch_single_pass(FusedArgs a, bool products, int compute_units, hipStream_t st) {
     const int64_t tiles = ceil_div(a.qb, 16);
     a.stages = a.r / kStage;
     const int64_t slots = (a.stages + 3) / 4 * 4;           // stage slots per tile, a multiple of four
@@ -414,6 +433,40 @@ hipError_t launch_fused_bf16(FusedArgs a, bool products, int compute_units, hipS
         hipLaunchKernelGGL((fused_bf16_kernel<kWaves, 24, 8, false>), dim3(static_cast<unsigned>(blocks)),
                            dim3(kWaves * 64), 0, st, a);
     return hipGetLastError();
+}
+
+}  // namespace
+
+bool fused_bf16_supported(int n, int k, int planes, int64_t r, int64_t lda) {
+    // a 64-row buffer of X^T and a 16-row tile of A must stay below 2^31 bytes
+    return planes == 2 && k == 24 && n - k == 8 && r > 0 && r % kStage == 0 && lda % 8 == 0 && r < (1 << 23) &&
+           lda < (1 << 25);
+}
+
+hipError_t launch_fused_bf16(FusedArgs a, bool products, int compute_units, hipStream_t st) {
+    if (a.qb == 0 || a.r == 0) return hipSuccess;
+    if (products) {
+        const int64_t ny = static_cast<int64_t>(a.n) * a.qb * 64;
+        hipLaunchKernelGGL(zero_f32_kernel, dim3(static_cast<unsigned>(ceil_div(ny, 4 * 256))), dim3(256), 0, st, a.Y,
+                           ny);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return launch_single_pass(a, products, compute_units, st);
+}
+
+hipError_t launch_fused_bf16_from_x(FusedArgs a, const uint16_t* X, int64_t s, int64_t ldx, int compute_units,
+                                    hipStream_t st) {
+    if (a.qb == 0 || a.r == 0) return hipSuccess;
+    const int64_t tiles_s = ceil_div(s, 64), ttiles = ceil_div(a.r, 64) * tiles_s;
+    const int64_t ny = static_cast<int64_t>(a.n) * a.qb * 64;
+    const int64_t blocks = ttiles + ceil_div(ny, 4096);
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(fused_prep_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, X, a.r, s, ldx,
+                       const_cast<uint16_t*>(a.xt), tiles_s, ttiles, a.Y, ny);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_single_pass(a, true, compute_units, st);
 }
 
 }  // namespace coded
