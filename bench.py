@@ -666,6 +666,16 @@ def dense_bf16_workload(args):
     for t in range(W):
         lib.coded_matmul(code, dA, par, dX[t], out[t], ws, info[t:t + 1], seed, t, parity_ready=False)
     torch.cuda.synchronize()
+    # The single pass is partly issue-bound, so it runs about 7% faster once
+    # the GPU's clocks have ramped under load (1.44 against 1.545 ms per pass
+    # after 0.5 s of calls): untimed calls for at least one second more, so the
+    # timed calls measure the steady state however short W is.
+    warm = [i % (K + W) for i in range(8)]           # draws and outputs the timed loop also uses
+    t_warm = time.perf_counter()
+    while time.perf_counter() - t_warm < 1.0:
+        for t in warm:
+            lib.coded_matmul(code, dA, par, dX[t], out[t], ws, info[t:t + 1], seed, t, parity_ready=False)
+        torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     start = time.perf_counter()
     for i in range(K):
