@@ -162,6 +162,24 @@ def blas_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
+# Compute- and latency-bound steps run faster once the GPU's clocks have
+# ramped under load (the dense single pass: 1.545 ms per pass after three
+# calls, 1.44 ms after half a second of them; the (4,2) one-launch product:
+# 7.33 against 7.21 us).  Those workloads call their step, untimed, for
+# CLOCK_RAMP_S before the timed steps, so that the timed steps measure the
+# steady state; the memory-bound GEMV workloads do not need it.
+CLOCK_RAMP_S = 1.0
+
+
+def ramp_clocks(call, seconds: float = CLOCK_RAMP_S) -> None:
+    import torch
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for i in range(8):
+            call(i)
+        torch.cuda.synchronize()
+
+
 def gemv_workload(args):
     import torch
 
@@ -386,6 +404,7 @@ def mds_small_workload(args):
     for t in range(W):
         step(t)
     torch.cuda.synchronize()
+    ramp_clocks(step)
     # Events only around the whole timed loop: per-step events would sit
     # between the launches (about 1.7 us each here).  Device time per product
     # is the loop's event interval over the steps.
@@ -440,6 +459,7 @@ def mds_small_workload(args):
                                   "sample": f"{cnt} coded products of the same seeds (encode, 4 worker products, "
                                             f"draw, LU decode) in {el:.1f} s",
                                   "gpu_vs_oracle_max_rel_err": worst}
+    result["clock_ramp_s"] = CLOCK_RAMP_S     # untimed calls before the timed steps
     return result
 
 
@@ -487,6 +507,7 @@ def decode_workload(args):
     for _ in range(W):
         lib.coded_decode_batched(code, dsets, Y, q, out, info)
     torch.cuda.synchronize()
+    ramp_clocks(lambda i: lib.coded_decode_batched(code, dsets, Y, q, out, info))
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     start = time.perf_counter()
     for i in range(K):
@@ -527,6 +548,7 @@ def decode_workload(args):
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(w, A, X, P, sets, out, args.cpu_decodes)
+    result["clock_ramp_s"] = CLOCK_RAMP_S     # untimed calls before the timed steps
     return result
 
 
@@ -666,16 +688,9 @@ def dense_bf16_workload(args):
     for t in range(W):
         lib.coded_matmul(code, dA, par, dX[t], out[t], ws, info[t:t + 1], seed, t, parity_ready=False)
     torch.cuda.synchronize()
-    # The single pass is partly issue-bound, so it runs about 7% faster once
-    # the GPU's clocks have ramped under load (1.44 against 1.545 ms per pass
-    # after 0.5 s of calls): untimed calls for at least one second more, so the
-    # timed calls measure the steady state however short W is.
-    warm = [i % (K + W) for i in range(8)]           # draws and outputs the timed loop also uses
-    t_warm = time.perf_counter()
-    while time.perf_counter() - t_warm < 1.0:
-        for t in warm:
-            lib.coded_matmul(code, dA, par, dX[t], out[t], ws, info[t:t + 1], seed, t, parity_ready=False)
-        torch.cuda.synchronize()
+    # draws and outputs the timed loop also uses
+    ramp_clocks(lambda i: lib.coded_matmul(code, dA, par, dX[i % (K + W)], out[i % (K + W)], ws,
+                                           info[i % (K + W):i % (K + W) + 1], seed, i % (K + W), parity_ready=False))
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     start = time.perf_counter()
     for i in range(K):
@@ -744,6 +759,7 @@ def dense_bf16_workload(args):
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_dense(w, A, Xs, P, W, out, code.qb(q), args.cpu_rows)
+    result["clock_ramp_s"] = CLOCK_RAMP_S     # untimed calls before the timed steps
     return result
 
 
@@ -790,6 +806,7 @@ def runtime_sim_workload(args):
     for t in range(W):
         lib.coded_simulate_runtimes(n, k, seed, t * draws, *out)
     torch.cuda.synchronize()
+    ramp_clocks(lambda i: lib.coded_simulate_runtimes(n, k, seed, (i % max(W, 1)) * draws, *out))
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     start = time.perf_counter()
     for i in range(K):
@@ -828,6 +845,7 @@ def runtime_sim_workload(args):
         result["cpu_baseline"] = {"value": cnt / el, "unit": "simulated draws/s", "cores": 1,
                                   "kind": "oracle", "sample": f"{cnt} draws of the same simulation with the NumPy "
                                                               f"oracle, {chunks} calls of {chunk}, in {el:.1f} s"}
+    result["clock_ramp_s"] = CLOCK_RAMP_S     # untimed calls before the timed steps
     return result
 
 
@@ -1122,7 +1140,8 @@ def main():
                 d["cpu_baseline"].update(host_info())
             result["dense_gemm"] = {key: d[key] for key in ("value", "unit", "steps", "warmup", "ms_per_step",
                                                             "dtype", "config", "call_ms_events", "encode_worker_ms",
-                                                            "call_hbm_frac", "roofline", "cpu_baseline") if key in d}
+                                                            "call_hbm_frac", "roofline", "cpu_baseline", "clock_ramp_s")
+                                   if key in d}
     if isinstance(result.get("cpu_baseline"), dict):
         result["cpu_baseline"].update(host_info())
     print(json.dumps(result), flush=True)
