@@ -377,14 +377,35 @@ __global__ void zero_f32_kernel(float* p, int64_t n) {
 // What the single pass with products needs before it starts, in one launch:
 // X (r x s bf16, row stride ldx) transposed into XT (s x r) by the first
 // `ttiles` workgroups, 64 x 64 tiles through LDS, and Y (ny floats) zeroed by
-// the others, 4096 floats each with 16-byte stores.
+// the others, 16384 floats each with 16-byte stores.  With vec (s = 64, r a
+// multiple of 64, X 16-byte aligned, ldx a multiple of 8) the tiles move in
+// 16-byte pieces; otherwise element by element.
 __global__ __launch_bounds__(256) void fused_prep_kernel(const uint16_t* __restrict__ X, int64_t r, int64_t s,
                                                          int64_t ldx, uint16_t* __restrict__ XT, int64_t tiles_s,
-                                                         int64_t ttiles, float* __restrict__ Y, int64_t ny) {
-    __shared__ uint16_t tile[64][65];
+                                                         int64_t ttiles, float* __restrict__ Y, int64_t ny, int vec) {
+    __shared__ uint16_t tile[64][72];            // rows of 144 bytes: 16-byte aligned pieces
     const int64_t bid = blockIdx.x;
     if (bid < ttiles) {
         const int64_t tr = bid / tiles_s, ts = bid % tiles_s;
+        if (vec) {
+            // 64 rows x 8 pieces of X in, 64 rows x 8 pieces of X^T out: two of each per thread
+            for (int p = threadIdx.x; p < 512; p += 256) {
+                const int i = p >> 3, j = p & 7;
+                *reinterpret_cast<uint4*>(&tile[i][8 * j]) =
+                    *reinterpret_cast<const uint4*>(X + (tr * 64 + i) * ldx + 8 * j);
+            }
+            __syncthreads();
+            for (int p = threadIdx.x; p < 512; p += 256) {
+                const int c = p >> 3, j = p & 7;
+                uint32_t w[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    w[u] = static_cast<uint32_t>(tile[8 * j + 2 * u][c]) |
+                           (static_cast<uint32_t>(tile[8 * j + 2 * u + 1][c]) << 16);
+                *reinterpret_cast<uint4*>(XT + c * r + tr * 64 + 8 * j) = uint4{w[0], w[1], w[2], w[3]};
+            }
+            return;
+        }
         const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
         for (int i = ty; i < 64; i += 4) {
             const int64_t k = tr * 64 + i, c = ts * 64 + tx;
@@ -397,9 +418,9 @@ __global__ __launch_bounds__(256) void fused_prep_kernel(const uint16_t* __restr
         }
         return;
     }
-    const int64_t base = (bid - ttiles) * 4096 + threadIdx.x * 4;
+    const int64_t base = (bid - ttiles) * 16384 + threadIdx.x * 4;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 16; ++u) {
         const int64_t i = base + u * 1024;
         if (i + 4 <= ny)
             *reinterpret_cast<f32x4f*>(Y + i) = f32x4f{0.f, 0.f, 0.f, 0.f};
@@ -460,10 +481,12 @@ hipError_t launch_fused_bf16_from_x(FusedArgs a, const uint16_t* X, int64_t s, i
     if (a.qb == 0 || a.r == 0) return hipSuccess;
     const int64_t tiles_s = ceil_div(s, 64), ttiles = ceil_div(a.r, 64) * tiles_s;
     const int64_t ny = static_cast<int64_t>(a.n) * a.qb * 64;
-    const int64_t blocks = ttiles + ceil_div(ny, 4096);
+    const int64_t blocks = ttiles + ceil_div(ny, 16384);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const int vec = s == 64 && a.r % 64 == 0 && ldx % 8 == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0 &&
+                    (reinterpret_cast<uintptr_t>(a.xt) & 15u) == 0;
     hipLaunchKernelGGL(fused_prep_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, X, a.r, s, ldx,
-                       const_cast<uint16_t*>(a.xt), tiles_s, ttiles, a.Y, ny);
+                       const_cast<uint16_t*>(a.xt), tiles_s, ttiles, a.Y, ny, vec);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_single_pass(a, true, compute_units, st);
