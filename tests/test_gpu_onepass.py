@@ -16,9 +16,10 @@ pytestmark = pytest.mark.gpu
 # (n, k, q, r): the configured (4,2) shape; padding rows (q % k != 0) with the
 # 64-thread variant; 260 columns (a partial chunk) with 128 threads; the
 # 256-thread variant over several column chunks; a single block row; the
-# widest code served
+# widest code served; three and two workers (the n <= 4 sums with absent
+# values)
 SHAPES = [(4, 2, 2048, 512), (5, 3, 31, 8), (6, 4, 1001, 260), (16, 12, 700, 1024), (7, 4, 3, 4),
-          (16, 8, 2000, 2048)]
+          (16, 8, 2000, 2048), (3, 2, 999, 132), (2, 1, 65, 64)]
 
 
 @pytest.fixture(scope="module")
