@@ -116,6 +116,25 @@ __device__ inline double quad_class_total(double v0, double v1, double v2, doubl
     return w;
 }
 
+// The same for eight values v[0..7]: exchanges 1 and 2 lanes apart and a
+// rotation by 4 halve them three times, so lane l keeps value
+// ((l & 1) << 2) | (l & 2) | ((l >> 2) & 1) summed over its half-row; a
+// rotation by 8 and permutes 16 and 32 lanes apart then add the rest.  Lane
+// l < 8 returns the total of that value.
+__device__ inline double octet_class_total(const double (&v)[8], int lane) {
+    const bool b0 = (lane & 1) != 0, b1 = (lane & 2) != 0, b2 = (lane & 4) != 0;
+    double z[4], w[2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) z[j] = (b0 ? v[j + 4] : v[j]) + dpp_f64<0xB1>(b0 ? v[j] : v[j + 4]);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) w[j] = (b1 ? z[j + 2] : z[j]) + dpp_f64<0x4E>(b1 ? z[j] : z[j + 2]);
+    double x = (b2 ? w[1] : w[0]) + dpp_f64<0x124>(b2 ? w[0] : w[1]);   // row_ror:4
+    x += dpp_f64<0x128>(x);                                             // row_ror:8
+    x += lane_xor(x, lane, 16);
+    x += lane_xor(x, lane, 32);
+    return x;
+}
+
 __device__ inline double dot4(f32x4o a, f32x4o x, double acc) {
     acc = fma(static_cast<double>(a.x), static_cast<double>(x.x), acc);
     acc = fma(static_cast<double>(a.y), static_cast<double>(x.y), acc);
@@ -248,6 +267,12 @@ __global__ __launch_bounds__(NT) void onepass_f32_kernel(OnePassArgs a) {
         const double v = quad_class_total(y[0], y[1], y[2], y[3], lane);
         const int i = ((lane & 1) << 1) | ((lane >> 1) & 1);
         if (lane < 4 && i < n) red[wv][i] = v;
+    } else if (n <= 8) {
+        // lane l < 8 holds the total of value ((l & 1) << 2) | (l & 2) | ((l >> 2) & 1)
+        const double y8[8] = {y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]};
+        const double v = octet_class_total(y8, lane);
+        const int i = ((lane & 1) << 2) | (lane & 2) | ((lane >> 2) & 1);
+        if (lane < 8 && i < n) red[wv][i] = v;
     } else {
 #pragma unroll
         for (int i = 0; i < MN; ++i) {
